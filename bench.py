@@ -1,0 +1,196 @@
+#!/usr/bin/env python3
+"""Benchmark: batched exemplar-clustering evaluation on one MI355X.
+
+One step = one call of the library on one batch: exemplar_eval (gather and
+norms of the exemplars, the fused contraction/min/sum kernel, the fixed-order
+second pass) for eval workloads, exemplar_gain (cache + scoring) for greedy
+workloads.  Inputs are synthetic, seeded, and resident in HBM before timing
+starts.  Prints one JSON line on stdout; progress goes to stderr.
+
+Default workload: 50 000 points of a 10-Gaussian mixture in d = 32 (fp32),
+256 sets of 10 exemplars.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import platform
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+from paper_2101_08763_amd import api, synth  # noqa: E402
+
+METRIC = "set evaluations/s and distance terms/s (n·k·l) + % of MFMA/HBM peak"
+PEAK_TFLOPS = {"fp32": 157.3, "fp16": 2516.6, "bf16": 2516.6}  # dense MFMA, MI355X
+DTYPE_NAME = {"fp32": "f32", "fp16": "f16", "bf16": "bf16"}
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def cpu_model() -> str:
+    try:
+        for ln in open("/proc/cpuinfo"):
+            if ln.startswith("model name"):
+                return ln.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.processor() or "unknown"
+
+
+def cpu_baseline(p: synth.Problem, X64: np.ndarray, budget_s: float):
+    """The oracle, as it stands, on the host cores, over a bounded sample of
+    the same workload (all sets when they fit in the budget)."""
+    import oracle
+
+    o = oracle.load()
+    w = p.workload
+    threads = o.threads(0)
+    if w.mode == "gain":
+        probe = p.cands[:1]
+        t0 = time.perf_counter()
+        o.gain(X64, p.S, probe, threads)
+        per = time.perf_counter() - t0
+        m = int(max(1, min(len(p.cands), budget_s / max(per, 1e-9))))
+        idx = np.unique((np.arange(m) * (len(p.cands) - 1)) // max(m - 1, 1))
+        t0 = time.perf_counter()
+        o.gain(X64, p.S, p.cands[idx], threads)
+        dt = time.perf_counter() - t0
+        kk = w.k + 1
+    else:
+        probe = p.sets[:min(len(p.sets), threads)]
+        t0 = time.perf_counter()
+        o.eval(X64, probe, threads)
+        per = (time.perf_counter() - t0) / len(probe)
+        m = int(max(1, min(len(p.sets), budget_s / max(per, 1e-9))))
+        idx = np.unique((np.arange(m) * (len(p.sets) - 1)) // max(m - 1, 1))
+        t0 = time.perf_counter()
+        o.eval(X64, p.sets[idx], threads)
+        dt = time.perf_counter() - t0
+        kk = w.k
+    m = len(idx)
+    sample = "all sets" if m == w.l else f"strided sample of {m} of {w.l} sets"
+    return {
+        "value": m / dt, "unit": "set evaluations/s", "cores": threads, "kind": "oracle",
+        "sample": f"{sample}, fp64 direct evaluation, OpenMP over sets, {threads} threads on {cpu_model()}",
+        "seconds": dt, "distance_terms_per_s": w.n * kk * m / dt,
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="mix50k", choices=sorted(synth.WORKLOADS))
+    ap.add_argument("--cpu-budget", type=float, default=10.0, help="seconds of oracle time for the CPU baseline")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); the library has no multi-GPU "
+              "path in this version.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    if not torch.cuda.is_available():
+        sys.exit("bench.py needs a GPU")
+    api.load()
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+
+    w = synth.WORKLOADS[args.workload]
+    log(f"generating {w.name}: {w.note}")
+    p = synth.make(w)
+    Xs, X64 = synth.rounded(p.X, w.precision)
+    V = (Xs if isinstance(Xs, torch.Tensor) else torch.from_numpy(Xs)).to(dev).contiguous()
+    if w.mode == "gain":
+        S = torch.from_numpy(p.S).to(dev)
+        C = torch.from_numpy(p.cands).to(dev)
+        out = torch.empty(w.l, dtype=torch.float32, device=dev)
+        step = lambda: api.exemplar_gain(V, S, C, out=out)  # noqa: E731
+        kk = w.k + 1
+        contraction_cols = w.l          # scoring kernel: n x l x d
+    else:
+        sets = torch.from_numpy(p.sets).to(dev)
+        out = torch.empty(w.l, dtype=torch.float32, device=dev)
+        step = lambda: api.exemplar_eval(V, sets, out=out)  # noqa: E731
+        kk = w.k
+        contraction_cols = w.l * w.k    # eval kernel: n x (l k) x d
+    prec_code = {"fp32": api.EXEMCL_FP32, "fp16": api.EXEMCL_FP16, "bf16": api.EXEMCL_BF16}[w.precision]
+    path, ws = api.exemplar_plan(w.n, w.d, w.l, w.k if w.mode == "eval" else 1, prec_code)
+    torch.cuda.synchronize()
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    api.exemplar_prof_read()  # drop anything recorded before
+
+    stream = torch.cuda.current_stream()
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    api.exemplar_prof_enable(True)
+    torch.cuda.synchronize()
+    ev0.record(stream)
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    api.exemplar_prof_enable(False)
+    kern_ms, launches = api.exemplar_prof_read()
+    ms = ev0.elapsed_time(ev1)
+    ms_per_step = ms / args.steps
+    kern_avg_ms = kern_ms / max(launches, 1)
+
+    value = w.l / (ms_per_step * 1e-3)
+    terms = w.n * kk * w.l
+    flops_per_launch = 2.0 * w.n * contraction_cols * w.d
+    achieved = flops_per_launch / (kern_avg_ms * 1e-3) / 1e12
+    peak = PEAK_TFLOPS[w.precision]
+    log(f"{args.steps} steps: {ms_per_step * 1e3:.1f} us/step (wall {wall / args.steps * 1e6:.1f} us/step), "
+        f"dominant kernel {kern_avg_ms * 1e3:.1f} us avg over {launches} launches, {achieved:.1f} TFLOP/s")
+
+    res = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "set evaluations/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": DTYPE_NAME[w.precision],
+        "data": "synthetic",
+        "distance_terms_per_s": terms / (ms_per_step * 1e-3),
+        "config": {
+            "workload": f"{w.name}: {w.note}", "n": w.n, "d": w.d, "l": w.l,
+            ("base_set" if w.mode == "gain" else "k"): w.k, "mode": w.mode,
+            "precision": w.precision, "seed": w.seed, "path": path, "workspace_bytes": ws,
+        },
+        "roofline": {
+            "bound": "mfma", "achieved": achieved, "peak": peak, "unit": "TFLOP/s", "frac": achieved / peak,
+            "traffic": None, "kernel": "eval_mfma_kernel" if path == "mfma" else "eval_valu_kernel",
+            "kernel_avg_us": kern_avg_ms * 1e3, "flops_per_launch": flops_per_launch,
+        },
+    }
+    if not args.no_cpu_baseline:
+        log(f"oracle baseline (budget {args.cpu_budget:.0f} s) ...")
+        res["cpu_baseline"] = cpu_baseline(p, X64, args.cpu_budget)
+        log(f"oracle: {res['cpu_baseline']['value']:.3g} set-evals/s on {res['cpu_baseline']['cores']} threads")
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

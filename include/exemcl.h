@@ -1,0 +1,172 @@
+/*
+ * exemcl.h -- C ABI of the MI355X exemplar-clustering evaluator.
+ *
+ * The library scores sets of exemplars under the exemplar-based clustering
+ * function of Buschjaeger & Morik ("GPU-Accelerated Optimizer-Aware
+ * Evaluation of Submodular Exemplar Clustering"):
+ *
+ *   L(X) = (1/n) * sum_{v in V} min_{x in X} ||v - x||^2        (Eq. (3))
+ *   f(S) = L({e0}) - L(S u {e0}),  e0 = the zero vector          (Eq. (4))
+ *
+ * with the squared Euclidean dissimilarity of the paper's experiments
+ * (Section V).  It evaluates many sets in one call, the "multiset" workload an
+ * optimizer produces in every step (Section IV-A), on one gfx950 GPU.
+ *
+ * Conventions shared by every entry point:
+ *   - Array arguments are DEVICE pointers on the current HIP device.  The
+ *     caller owns them and keeps them alive until the work queued on `stream`
+ *     has finished; the library only reads its inputs and writes its outputs.
+ *   - `stream` is a hipStream_t (NULL = the null stream).  Calls are
+ *     asynchronous: they validate on the host, queue kernels on `stream` and
+ *     return without synchronising.  Temporary device memory comes from a
+ *     library-owned stream-ordered pool and is released in stream order
+ *     before the call returns.  Nothing persists between calls except that
+ *     pool.  Calls on different streams may run concurrently.
+ *   - V is dense row-major n x d (row stride d elements, no padding), with
+ *     element type fp32, fp16 or bf16 as selected by `precision`.  Results are
+ *     fp32.  Arithmetic is fp32 (fp16/bf16 products are exact in fp32).
+ *   - Sets are int32 row indices into V.  Duplicate indices are allowed.  An
+ *     index outside [0, n) makes that set's result a quiet NaN and leaves the
+ *     other results untouched (detected on the device, no sync).
+ *   - The return value is a status, decided on the host before any kernel
+ *     runs (EINVAL, ENOMEM) or right after the launches (EDEVICE).
+ *   - Every result is bitwise reproducible and independent of the batch it
+ *     came in: out[j] depends on V and on set j only, not on l, j or the
+ *     other sets.
+ */
+#ifndef EXEMCL_H
+#define EXEMCL_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#if defined(__GNUC__)
+#define EXEMCL_API __attribute__((visibility("default")))
+#else
+#define EXEMCL_API
+#endif
+
+/* Storage type of V. */
+enum exemcl_precision { EXEMCL_FP32 = 0, EXEMCL_FP16 = 1, EXEMCL_BF16 = 2 };
+
+/* Status codes. */
+enum exemcl_status {
+    EXEMCL_OK = 0,      /* queued (or nothing to do) */
+    EXEMCL_EINVAL = 1,  /* bad argument; nothing was queued */
+    EXEMCL_ENOMEM = 2,  /* temporary device memory unavailable; nothing was queued */
+    EXEMCL_EDEVICE = 3  /* a HIP call or kernel launch failed */
+};
+
+/* Evaluation paths (see exemplar_plan). */
+enum exemcl_path {
+    EXEMCL_PATH_NONE = 0, /* nothing to launch (l == 0 or k == 0) */
+    EXEMCL_PATH_VALU = 1, /* vector-ALU kernel, exemplars staged in LDS (small d) */
+    EXEMCL_PATH_MFMA = 2  /* matrix-core contraction with fused min/sum epilogue */
+};
+
+/*
+ * exemplar_eval -- f(S_j) for a batch of l sets of k exemplars each.
+ *
+ * Computes out[j] = f(S_j) = L({e0}) - L(S_j u {e0}) (Eq. (3), Eq. (4)) for
+ * S_j = { V[sets[j*k + p]] : p < k }, the multiset evaluation of Section IV-A.
+ * Internally the value is formed as (2/n) * sum_v max(0, max_{s in S_j}
+ * (<v,s> - ||s||^2/2)), which equals the definition exactly in real
+ * arithmetic and avoids subtracting two nearly equal losses.
+ *
+ *   V          device, n x d row-major, type per `precision`; read only
+ *   n          number of ground points, 1 <= n <= INT32_MAX
+ *   d          dimension, 1 <= d <= 512 (larger d: EINVAL in this version)
+ *   sets       device, l x k int32 row-major; read only (may be NULL if k == 0)
+ *   l          number of sets, l >= 0 (l == 0: returns EXEMCL_OK, queues nothing)
+ *   k          set size, k >= 0 (k == 0: every out[j] = 0, since f(empty) = 0)
+ *   precision  one of exemcl_precision
+ *   out        device, l floats; written
+ *   stream     hipStream_t or NULL
+ *
+ * Errors: EINVAL for a NULL array with a non-zero size, n < 1, n > INT32_MAX,
+ * d < 1, d > 512, k < 0, l < 0 or an unknown precision; ENOMEM when the temporary
+ * buffers (partial sums and staged exemplar tiles, O(l*k*d) bytes) cannot be
+ * allocated -- the analogue of the paper's chunking failure (Section IV-B,
+ * Chunking); EDEVICE when a launch fails.
+ */
+EXEMCL_API int exemplar_eval(const void *V, int64_t n, int64_t d, const int32_t *sets, int64_t l,
+                             int64_t k, int precision, float *out, void *stream);
+
+/*
+ * exemplar_gain -- one Greedy step: f(S u {c}) for every candidate c.
+ *
+ * The Greedy optimizer (Algorithm 1) evaluates, in every round, the multiset
+ * { S u {c_1}, ..., S u {c_m} } for the current solution S (Section IV-A).
+ * This call scores that multiset with fp32 V: it first caches, for every
+ * point, g(v) = max(0, max_{s in S} (<v,s> - ||s||^2/2)) (so that
+ * min(||v||^2, min_s ||v-s||^2) = ||v||^2 - 2 g(v)), then forms
+ * out[j] = (2/n) * sum_v max(g(v), <v,c_j> - ||c_j||^2/2) = f(S u {c_j}).
+ * The discrete derivative of Definition 1 is out[j] - f(S).
+ *
+ *   V      device, n x d fp32 row-major; read only
+ *   n, d   as for exemplar_eval
+ *   S      device, k int32 indices (the current solution); NULL if k == 0
+ *   k      |S| >= 0; every scored set has k + 1 members
+ *   cands  device, l int32 candidate indices; read only
+ *   l      number of candidates, l >= 0
+ *   out    device, l floats; written
+ *   stream hipStream_t or NULL
+ *
+ * A candidate already in S scores f(S).  An invalid index in S makes every
+ * result NaN; an invalid candidate makes its own result NaN.
+ * Errors as for exemplar_eval.
+ */
+EXEMCL_API int exemplar_gain(const float *V, int64_t n, int64_t d, const int32_t *S, int64_t k,
+                             const int32_t *cands, int64_t l, float *out, void *stream);
+
+/*
+ * exemplar_sqnorm -- q[i] = ||v_i||^2, the squared distance of every ground
+ * point to e0, in fp32.  Its mean is L({e0}), the set-independent term of
+ * Eq. (4) that the paper computes once up front (Section IV-B, Algorithm).
+ *
+ *   V, n, d, precision  as for exemplar_eval
+ *   q                   device, n floats; written
+ *
+ * Errors: EINVAL / EDEVICE as above.
+ */
+EXEMCL_API int exemplar_sqnorm(const void *V, int64_t n, int64_t d, int precision, float *q,
+                               void *stream);
+
+/*
+ * exemplar_plan -- host-only description of what exemplar_eval would launch
+ * for these sizes; touches no device.  Writes the chosen exemcl_path to
+ * *path and the temporary device bytes to *workspace_bytes (either pointer
+ * may be NULL).  The path depends on (d, k, precision) only, never on l or n,
+ * which is what keeps out[j] independent of the batch.  The environment
+ * variable EXEMCL_PATH=valu|mfma forces a path where it applies (tests).
+ * Returns EINVAL for arguments exemplar_eval would reject, else EXEMCL_OK.
+ */
+EXEMCL_API int exemplar_plan(int64_t n, int64_t d, int64_t l, int64_t k, int precision, int *path,
+                             int64_t *workspace_bytes);
+
+/*
+ * Profiling hook.  exemplar_prof_enable(1) makes every following
+ * exemplar_eval / exemplar_gain call record a pair of HIP events on its
+ * stream around its dominant kernel (the contraction + epilogue kernel);
+ * exemplar_prof_enable(0) stops recording.  exemplar_prof_read waits for the
+ * recorded events, writes the summed kernel time in milliseconds and the
+ * number of recorded launches, and forgets them.  Either pointer may be NULL.
+ * Meant for benchmarks; recording costs two event records per call.
+ */
+EXEMCL_API int exemplar_prof_enable(int on);
+EXEMCL_API int exemplar_prof_read(double *ms_total, int64_t *launches);
+
+/* exemplar_strerror -- static, NUL-terminated text for a status code. */
+EXEMCL_API const char *exemplar_strerror(int status);
+
+/* exemplar_version -- library version as 10000*major + 100*minor + patch. */
+EXEMCL_API int exemplar_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* EXEMCL_H */

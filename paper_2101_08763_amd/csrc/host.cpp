@@ -1,0 +1,348 @@
+// host.cpp -- the C ABI declared in include/exemcl.h: argument validation,
+// path selection, stream-ordered temporary memory, kernel sequencing.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#include <mutex>
+#include <utility>
+#include <vector>
+
+#include "exemcl.h"
+#include "internal.h"
+
+using namespace exemcl;
+
+namespace {
+
+constexpr int kVersion = 100;  // 0.1.0
+
+bool prec_ok(int p) { return p == EXEMCL_FP32 || p == EXEMCL_FP16 || p == EXEMCL_BF16; }
+
+int64_t align_up(int64_t x, int64_t a) { return (x + a - 1) / a * a; }
+
+// EXEMCL_PATH=valu|mfma forces a path where it applies (tests, tuning).
+int forced_path() {
+    const char *s = getenv("EXEMCL_PATH");
+    if (!s) return 0;
+    if (!strcmp(s, "valu")) return EXEMCL_PATH_VALU;
+    if (!strcmp(s, "mfma")) return EXEMCL_PATH_MFMA;
+    return 0;
+}
+
+// EXEMCL_WORKSPACE_LIMIT=<bytes> caps temporary memory (forces ENOMEM in tests).
+int64_t workspace_limit() {
+    const char *s = getenv("EXEMCL_WORKSPACE_LIMIT");
+    if (!s || !*s) return INT64_MAX;
+    char *end = nullptr;
+    long long v = strtoll(s, &end, 10);
+    return (end && *end == '\0' && v >= 0) ? (int64_t)v : INT64_MAX;
+}
+
+// Path choice: a function of (d, k, precision) only.
+int choose_path(int64_t d, int64_t k, int precision) {
+    MfmaPlan mp;
+    ValuPlan vp;
+    const bool can_mfma = mfma_plan(precision, d, &mp);
+    const bool can_valu = valu_plan(precision, d, k, &vp);
+    const int f = forced_path();
+    if (f == EXEMCL_PATH_VALU && can_valu) return EXEMCL_PATH_VALU;
+    if (f == EXEMCL_PATH_MFMA && can_mfma) return EXEMCL_PATH_MFMA;
+    if (can_mfma) return EXEMCL_PATH_MFMA;
+    if (can_valu) return EXEMCL_PATH_VALU;
+    return EXEMCL_PATH_NONE;
+}
+
+struct Layout {
+    int path = EXEMCL_PATH_NONE;
+    MfmaPlan mp{};
+    ValuPlan vp{};
+    int64_t G = 0, lpad = 0, ngroups = 0, gpc = 0;
+    int64_t off_partials = 0, off_tiles = 0, off_bias = 0, off_aux = 0, bytes = 0;
+};
+
+int64_t tile_bytes(const MfmaPlan &mp) { return (int64_t)mp.nkb * 64 * 16; }
+
+// Workspace of one exemplar_eval call (or of the scoring half of a gain call).
+bool layout_eval(int64_t n, int64_t d, int64_t l, int64_t k, int precision, int path, Layout *L) {
+    L->path = path;
+    if (path == EXEMCL_PATH_MFMA) {
+        if (!mfma_plan(precision, d, &L->mp)) return false;
+        const int64_t tm = L->mp.tile;
+        L->ngroups = (l + tm - 1) / tm;
+        L->lpad = L->ngroups * tm;
+        L->G = (n + L->mp.rows - 1) / L->mp.rows;
+        // Enough workgroups to cover 256 CUs several times; a chunk of set
+        // groups shares one load of the workgroup's points.
+        int64_t chunks = (2048 + L->G - 1) / L->G;
+        if (chunks < 1) chunks = 1;
+        if (chunks > L->ngroups) chunks = L->ngroups;
+        if (chunks > 65535) chunks = 65535;
+        L->gpc = (L->ngroups + chunks - 1) / chunks;
+        L->off_partials = 0;
+        L->off_tiles = align_up(L->G * L->lpad * 4, 256);
+        L->off_bias = align_up(L->off_tiles + L->ngroups * k * tile_bytes(L->mp), 256);
+        L->off_aux = align_up(L->off_bias + L->ngroups * k * tm * 4, 256);
+        L->bytes = L->off_aux;
+        return true;
+    }
+    if (path == EXEMCL_PATH_VALU) {
+        if (!valu_plan(precision, d, k, &L->vp)) return false;
+        L->lpad = l;
+        L->G = (n + L->vp.rows - 1) / L->vp.rows;
+        L->off_partials = 0;
+        L->off_aux = align_up(L->G * L->lpad * 4, 256);
+        L->bytes = L->off_aux;
+        return true;
+    }
+    L->bytes = 0;
+    return true;
+}
+
+int check_common(const void *V, int64_t n, int64_t d, int64_t l, int64_t k, const void *out) {
+    if (!V) return EXEMCL_EINVAL;
+    if (n < 1 || n > INT32_MAX) return EXEMCL_EINVAL;
+    if (d < 1 || d > INT32_MAX) return EXEMCL_EINVAL;
+    if (k < 0 || l < 0) return EXEMCL_EINVAL;
+    if (l > 0 && !out) return EXEMCL_EINVAL;
+    return EXEMCL_OK;
+}
+
+// Library-owned stream-ordered pool per device, keeping freed blocks cached.
+std::mutex g_pool_mu;
+hipMemPool_t g_pools[64] = {};
+
+hipError_t get_pool(hipMemPool_t *pool) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lk(g_pool_mu);
+    if (!g_pools[dev]) {
+        hipMemPoolProps props{};
+        props.allocType = hipMemAllocationTypePinned;
+        props.handleTypes = hipMemHandleTypeNone;
+        props.location.type = hipMemLocationTypeDevice;
+        props.location.id = dev;
+        hipMemPool_t p = nullptr;
+        e = hipMemPoolCreate(&p, &props);
+        if (e != hipSuccess) return e;
+        uint64_t keep = UINT64_MAX;
+        e = hipMemPoolSetAttribute(p, hipMemPoolAttrReleaseThreshold, &keep);
+        if (e != hipSuccess) return e;
+        g_pools[dev] = p;
+    }
+    *pool = g_pools[dev];
+    return hipSuccess;
+}
+
+struct Scratch {
+    void *ptr = nullptr;
+    hipStream_t st = nullptr;
+    ~Scratch() {
+        if (ptr) hipFreeAsync(ptr, st);
+    }
+};
+
+int alloc_scratch(Scratch *s, int64_t bytes, hipStream_t st) {
+    s->st = st;
+    if (bytes <= 0) return EXEMCL_OK;
+    if (bytes > workspace_limit()) return EXEMCL_ENOMEM;
+    hipMemPool_t pool;
+    if (get_pool(&pool) != hipSuccess) return EXEMCL_EDEVICE;
+    hipError_t e = hipMallocFromPoolAsync(&s->ptr, (size_t)bytes, pool, st);
+    if (e == hipErrorOutOfMemory) {
+        (void)hipGetLastError();
+        s->ptr = nullptr;
+        return EXEMCL_ENOMEM;
+    }
+    if (e != hipSuccess) {
+        s->ptr = nullptr;
+        return EXEMCL_EDEVICE;
+    }
+    return EXEMCL_OK;
+}
+
+int status_of(hipError_t e) { return e == hipSuccess ? EXEMCL_OK : EXEMCL_EDEVICE; }
+
+// Event pairs around the dominant kernel, recorded while profiling is on.
+std::mutex g_prof_mu;
+bool g_prof_on = false;
+std::vector<std::pair<hipEvent_t, hipEvent_t>> g_prof_events;
+
+struct ProfRange {
+    hipEvent_t a = nullptr, b = nullptr;
+    hipStream_t st;
+    explicit ProfRange(hipStream_t s) : st(s) {
+        bool on;
+        {
+            std::lock_guard<std::mutex> lk(g_prof_mu);
+            on = g_prof_on;
+        }
+        if (!on) return;
+        if (hipEventCreate(&a) != hipSuccess || hipEventCreate(&b) != hipSuccess) {
+            if (a) hipEventDestroy(a);
+            a = b = nullptr;
+            return;
+        }
+        hipEventRecord(a, st);
+    }
+    void end() {
+        if (!a) return;
+        hipEventRecord(b, st);
+        std::lock_guard<std::mutex> lk(g_prof_mu);
+        g_prof_events.emplace_back(a, b);
+        a = b = nullptr;
+    }
+    ~ProfRange() {
+        if (a) hipEventDestroy(a);
+        if (b) hipEventDestroy(b);
+    }
+};
+
+// Queue one evaluation of `l` sets of `k` members (shared by eval and the
+// scoring half of gain).  `m0` (nullable) is the per-point initial max.
+int run_eval(const void *V, int64_t n, int64_t d, const int32_t *sets, int64_t l, int64_t k, int precision,
+             const float *m0, const int32_t *common, int64_t kcommon, float *out, hipStream_t st) {
+    if (l == 0) return EXEMCL_OK;
+    int path = k == 0 ? EXEMCL_PATH_NONE : choose_path(d, k, precision);
+    if (m0 && path == EXEMCL_PATH_VALU) path = EXEMCL_PATH_MFMA;
+    if (k > 0 && path == EXEMCL_PATH_NONE) return EXEMCL_EINVAL;
+    Layout L;
+    if (!layout_eval(n, d, l, k, precision, path, &L)) return EXEMCL_EINVAL;
+    Scratch ws;
+    int rc = alloc_scratch(&ws, L.bytes, st);
+    if (rc) return rc;
+    char *base = (char *)ws.ptr;
+    float *partials = (float *)(base + L.off_partials);
+    hipError_t e = hipSuccess;
+    if (path == EXEMCL_PATH_MFMA) {
+        void *tiles = base + L.off_tiles;
+        float *bias = (float *)(base + L.off_bias);
+        e = launch_pack(precision, L.mp, V, n, (int)d, sets, l, k, tiles, bias, st);
+        if (e == hipSuccess) {
+            ProfRange pr(st);
+            e = launch_mfma(precision, MODE_SUM, L.mp, V, n, (int)d, tiles, bias, k, L.ngroups, L.gpc, m0, partials,
+                            L.lpad, nullptr, st);
+            pr.end();
+        }
+    } else if (path == EXEMCL_PATH_VALU) {
+        ProfRange pr(st);
+        e = launch_valu(precision, L.vp, V, n, (int)d, sets, l, k, partials, L.lpad, st);
+        pr.end();
+    }
+    if (e == hipSuccess) e = launch_reduce(partials, L.G, L.lpad, l, n, sets, k, common, kcommon, out, st);
+    return status_of(e);
+}
+
+}  // namespace
+
+extern "C" {
+
+EXEMCL_API int exemplar_eval(const void *V, int64_t n, int64_t d, const int32_t *sets, int64_t l, int64_t k,
+                             int precision, float *out, void *stream) {
+    int rc = check_common(V, n, d, l, k, out);
+    if (rc) return rc;
+    if (!prec_ok(precision)) return EXEMCL_EINVAL;
+    if (l > 0 && k > 0 && !sets) return EXEMCL_EINVAL;
+    if (l > 0 && k > 0 && choose_path(d, k, precision) == EXEMCL_PATH_NONE) return EXEMCL_EINVAL;
+    return run_eval(V, n, d, sets, l, k, precision, nullptr, nullptr, 0, out, (hipStream_t)stream);
+}
+
+EXEMCL_API int exemplar_gain(const float *V, int64_t n, int64_t d, const int32_t *S, int64_t k,
+                             const int32_t *cands, int64_t l, float *out, void *stream) {
+    int rc = check_common(V, n, d, l, k, out);
+    if (rc) return rc;
+    if (k > 0 && !S) return EXEMCL_EINVAL;
+    if (l > 0 && !cands) return EXEMCL_EINVAL;
+    MfmaPlan mp;
+    if (!mfma_plan(EXEMCL_FP32, d, &mp)) return EXEMCL_EINVAL;
+    if (l == 0) return EXEMCL_OK;
+    hipStream_t st = (hipStream_t)stream;
+    if (k == 0) return run_eval(V, n, d, cands, l, 1, EXEMCL_FP32, nullptr, nullptr, 0, out, st);
+
+    // Cache g(v) = max(0, max_{s in S} h_s(v)): S's members as single-member
+    // "sets" staged side by side, reduced by max over columns per point.
+    const int64_t tm = mp.tile;
+    const int64_t ngroups = (k + tm - 1) / tm;
+    const int64_t off_tiles = align_up(n * 4, 256);
+    const int64_t off_bias = align_up(off_tiles + ngroups * tile_bytes(mp), 256);
+    const int64_t bytes = align_up(off_bias + ngroups * tm * 4, 256);
+    Scratch ws;
+    rc = alloc_scratch(&ws, bytes, st);
+    if (rc) return rc;
+    char *base = (char *)ws.ptr;
+    float *gcache = (float *)base;
+    void *tiles = base + off_tiles;
+    float *bias = (float *)(base + off_bias);
+    hipError_t e = launch_pack(EXEMCL_FP32, mp, V, n, (int)d, S, k, 1, tiles, bias, st);
+    if (e == hipSuccess)
+        e = launch_mfma(EXEMCL_FP32, MODE_ROWMAX, mp, V, n, (int)d, tiles, bias, 1, ngroups, ngroups, nullptr,
+                        nullptr, 0, gcache, st);
+    if (e != hipSuccess) return EXEMCL_EDEVICE;
+    // Score every S u {c}: single-member sets {c} with the running max
+    // started at g(v) instead of e0's 0.
+    return run_eval(V, n, d, cands, l, 1, EXEMCL_FP32, gcache, S, k, out, st);
+}
+
+EXEMCL_API int exemplar_sqnorm(const void *V, int64_t n, int64_t d, int precision, float *q, void *stream) {
+    if (!V || !q) return EXEMCL_EINVAL;
+    if (n < 1 || n > INT32_MAX || d < 1 || d > INT32_MAX) return EXEMCL_EINVAL;
+    if (!prec_ok(precision)) return EXEMCL_EINVAL;
+    return status_of(launch_sqnorm(precision, V, n, (int)d, q, (hipStream_t)stream));
+}
+
+EXEMCL_API int exemplar_plan(int64_t n, int64_t d, int64_t l, int64_t k, int precision, int *path,
+                             int64_t *workspace_bytes) {
+    if (n < 1 || n > INT32_MAX || d < 1 || d > INT32_MAX || k < 0 || l < 0 || !prec_ok(precision))
+        return EXEMCL_EINVAL;
+    int p = (l == 0 || k == 0) ? EXEMCL_PATH_NONE : choose_path(d, k, precision);
+    if (l > 0 && k > 0 && p == EXEMCL_PATH_NONE) return EXEMCL_EINVAL;
+    Layout L;
+    if (!layout_eval(n, d, l, k, precision, p, &L)) return EXEMCL_EINVAL;
+    if (path) *path = p;
+    if (workspace_bytes) *workspace_bytes = L.bytes;
+    return EXEMCL_OK;
+}
+
+EXEMCL_API int exemplar_prof_enable(int on) {
+    std::lock_guard<std::mutex> lk(g_prof_mu);
+    g_prof_on = on != 0;
+    return EXEMCL_OK;
+}
+
+EXEMCL_API int exemplar_prof_read(double *ms_total, int64_t *launches) {
+    std::vector<std::pair<hipEvent_t, hipEvent_t>> ev;
+    {
+        std::lock_guard<std::mutex> lk(g_prof_mu);
+        ev.swap(g_prof_events);
+    }
+    double total = 0.0;
+    int rc = EXEMCL_OK;
+    for (auto &pr : ev) {
+        float ms = 0.0f;
+        if (hipEventSynchronize(pr.second) != hipSuccess || hipEventElapsedTime(&ms, pr.first, pr.second) != hipSuccess)
+            rc = EXEMCL_EDEVICE;
+        total += ms;
+        hipEventDestroy(pr.first);
+        hipEventDestroy(pr.second);
+    }
+    if (ms_total) *ms_total = total;
+    if (launches) *launches = (int64_t)ev.size();
+    return rc;
+}
+
+EXEMCL_API const char *exemplar_strerror(int status) {
+    switch (status) {
+    case EXEMCL_OK: return "success";
+    case EXEMCL_EINVAL: return "invalid argument";
+    case EXEMCL_ENOMEM: return "temporary device memory unavailable";
+    case EXEMCL_EDEVICE: return "HIP runtime or kernel launch failure";
+    }
+    return "unknown status";
+}
+
+EXEMCL_API int exemplar_version(void) { return kVersion; }
+
+}  // extern "C"

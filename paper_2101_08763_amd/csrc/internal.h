@@ -1,0 +1,66 @@
+// internal.h -- host-side launch interface between the ABI layer and the
+// kernel translation units.  Not installed; not part of the C ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace exemcl {
+
+enum Prec { P_FP32 = 0, P_FP16 = 1, P_BF16 = 2 };
+
+// Geometry of one MFMA evaluation launch; a pure function of (d, precision),
+// never of n or l, so that the partial-sum layout seen by one set does not
+// depend on the batch it arrives in.
+struct MfmaPlan {
+    int tile;       // TM: sets per column tile (32 or 16)
+    int kbmax;      // compile-time k-block capacity of the kernel
+    int nkb;        // k-blocks actually used, ceil(d / kb_dims)
+    int nks;        // MFMA instructions per tile, ceil(d / kstep)
+    int rt;         // row tiles per wavefront
+    int waves;      // wavefronts per workgroup
+    int rows;       // rows per workgroup = waves * rt * tile
+    int kb_dims;    // coordinates per k-block
+};
+
+bool mfma_plan(int prec, int64_t d, MfmaPlan *p);
+
+// Geometry of one VALU evaluation launch.
+struct ValuPlan {
+    int dp;         // padded dimension held in registers (1, 2, 4, 8, 16)
+    int rpt;        // rows per thread
+    int rows;       // rows per workgroup = 256 * rpt
+    int rec;        // floats per staged exemplar record (bias + dp coords, padded to 4)
+    int sets_per_chunk;
+};
+
+bool valu_plan(int prec, int64_t d, int64_t k, ValuPlan *p);
+
+// Stage the exemplar tiles of `l` sets of `k` indices: for every (set group,
+// slot) pair one TM-column tile of B lane vectors and one TM-vector of
+// biases -||s||^2/2 (-FLT_MAX for padding columns and invalid indices).
+hipError_t launch_pack(int prec, const MfmaPlan &pl, const void *V, int64_t n, int d, const int32_t *sets,
+                       int64_t l, int64_t k, void *tiles, float *bias, hipStream_t st);
+
+// Mode of the MFMA kernel's epilogue.
+enum Mode { MODE_SUM = 0, MODE_ROWMAX = 1 };
+
+// partials[rb * lpad + j] = sum over the rows of block rb of
+// max(m0(v), max_p (<v, s_jp> - ||s_jp||^2 / 2)); m0 = 0 when null.
+// MODE_ROWMAX instead writes rowmax[v] = max(0, max over all staged columns).
+hipError_t launch_mfma(int prec, int mode, const MfmaPlan &pl, const void *V, int64_t n, int d,
+                       const void *tiles, const float *bias, int64_t k, int64_t ngroups, int64_t groups_per_chunk,
+                       const float *m0, float *partials, int64_t lpad, float *rowmax, hipStream_t st);
+
+hipError_t launch_valu(int prec, const ValuPlan &pl, const void *V, int64_t n, int d, const int32_t *sets,
+                       int64_t l, int64_t k, float *partials, int64_t lpad, hipStream_t st);
+
+// out[j] = (2/n) * sum_g partials[g * lpad + j] (fp64, fixed order), or NaN
+// when an index of set j (or of the common list) is outside [0, n).
+hipError_t launch_reduce(const float *partials, int64_t G, int64_t lpad, int64_t l, int64_t n,
+                         const int32_t *sets, int64_t kset, const int32_t *common, int64_t kcommon,
+                         float *out, hipStream_t st);
+
+hipError_t launch_sqnorm(int prec, const void *V, int64_t n, int d, float *q, hipStream_t st);
+
+}  // namespace exemcl

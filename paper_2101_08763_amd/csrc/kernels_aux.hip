@@ -1,0 +1,240 @@
+// kernels_aux.hip -- vector-ALU evaluation for small d, the fixed-order
+// reduction of partial sums, squared norms and a fill kernel.
+#include <float.h>
+#include <math.h>
+
+#include "device.hpp"
+#include "internal.h"
+
+namespace exemcl {
+
+// ---------------------------------------------------------------------------
+// VALU evaluation (small d).
+//
+// Each thread keeps RPT ground points in registers (fp32, zero-padded to DP
+// coordinates).  The exemplars of a chunk of sets are gathered once per
+// workgroup into LDS as records [bias, s_0 .. s_{DP-1}] (bias = -||s||^2/2),
+// and every wavefront reads them with uniform addresses (broadcast).  Per
+// (point, set): m = max(m0, max_p (b_p + <v, s_p>)), the clamp form of
+// min(||v||^2, min_p ||v - s_p||^2).  The per-thread sum over its points is
+// reduced across the wavefront with a fixed xor tree and across the 4
+// wavefronts in fixed order into partials[rb][j].
+// ---------------------------------------------------------------------------
+template <typename T, int DP, int RPT>
+__global__ __launch_bounds__(256) void eval_valu_kernel(const T *__restrict__ V, int64_t n, int d,
+                                                         const int32_t *__restrict__ sets, int64_t l, int64_t k,
+                                                         int sets_per_chunk, float *__restrict__ partials,
+                                                         int64_t lpad) {
+    constexpr int REC = ((DP + 1) + 3) / 4 * 4;
+    extern __shared__ __align__(16) float ex[];
+    float *red = ex + (int64_t)sets_per_chunk * k * REC;  // [4][sets_per_chunk]
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int64_t rb = blockIdx.x;
+    const int64_t j0 = (int64_t)blockIdx.y * sets_per_chunk;
+    const int nsets = (int)min((int64_t)sets_per_chunk, l - j0);
+
+    // Stage the chunk's exemplars: one record per (set, member).
+    for (int64_t e = tid; e < (int64_t)nsets * k; e += 256) {
+        const int64_t jj = e / k, p = e - (e / k) * k;
+        const int64_t idx = sets[(j0 + jj) * k + p];
+        float *rec = ex + e * REC;
+        if (idx >= 0 && idx < n) {
+            const T *row = V + idx * (int64_t)d;
+            float q = 0.0f;
+            for (int t = 0; t < DP; ++t) {
+                const float x = t < d ? to_f32(row[t]) : 0.0f;
+                rec[1 + t] = x;
+                q = fmaf(x, x, q);
+            }
+            rec[0] = -0.5f * q;
+        } else {
+            for (int t = 0; t < DP; ++t) rec[1 + t] = 0.0f;
+            rec[0] = -FLT_MAX;
+        }
+    }
+
+    float v[RPT][DP];
+#pragma unroll
+    for (int r = 0; r < RPT; ++r) {
+        const int64_t i = rb * (256 * RPT) + r * 256 + tid;
+#pragma unroll
+        for (int t = 0; t < DP; ++t) v[r][t] = (i < n && t < d) ? to_f32(V[i * (int64_t)d + t]) : 0.0f;
+    }
+    __syncthreads();
+
+    for (int jj = 0; jj < nsets; ++jj) {
+        float m[RPT];
+#pragma unroll
+        for (int r = 0; r < RPT; ++r) m[r] = 0.0f;
+        const float *recs = ex + (int64_t)jj * k * REC;
+        for (int64_t p = 0; p < k; ++p) {
+            const float *rec = recs + p * REC;
+            float s[REC];
+#pragma unroll
+            for (int q = 0; q < REC; q += 4) {
+                const float4 w = *reinterpret_cast<const float4 *>(rec + q);
+                s[q] = w.x;
+                s[q + 1] = w.y;
+                s[q + 2] = w.z;
+                s[q + 3] = w.w;
+            }
+#pragma unroll
+            for (int r = 0; r < RPT; ++r) {
+                float h = s[0];
+#pragma unroll
+                for (int t = 0; t < DP; ++t) h = fmaf(v[r][t], s[1 + t], h);
+                m[r] = fmaxf(m[r], h);
+            }
+        }
+        float sum = m[0];
+#pragma unroll
+        for (int r = 1; r < RPT; ++r) sum += m[r];
+#pragma unroll
+        for (int off = 32; off >= 1; off >>= 1) sum += __shfl_xor(sum, off);
+        if (lane == 0) red[wave * sets_per_chunk + jj] = sum;
+    }
+    __syncthreads();
+    for (int jj = tid; jj < nsets; jj += 256) {
+        const float tot = ((red[jj] + red[sets_per_chunk + jj]) + red[2 * sets_per_chunk + jj]) +
+                          red[3 * sets_per_chunk + jj];
+        partials[rb * lpad + j0 + jj] = tot;
+    }
+}
+
+bool valu_plan(int prec, int64_t d, int64_t k, ValuPlan *p) {
+    (void)prec;
+    if (d < 1 || d > 16 || k < 1) return false;
+    ValuPlan q{};
+    q.dp = d <= 1 ? 1 : d <= 2 ? 2 : d <= 4 ? 4 : d <= 8 ? 8 : 16;
+    q.rpt = 4;
+    q.rows = 256 * q.rpt;
+    q.rec = ((q.dp + 1) + 3) / 4 * 4;
+    const int64_t budget = 48 * 1024;
+    const int64_t per_set = k * q.rec * (int64_t)sizeof(float) + 4 * sizeof(float);
+    int64_t spc = budget / per_set;
+    if (spc < 1) return false;
+    if (spc > 64) spc = 64;
+    q.sets_per_chunk = (int)spc;
+    *p = q;
+    return true;
+}
+
+template <typename T, int DP>
+static hipError_t valu_t(const ValuPlan &pl, const void *V, int64_t n, int d, const int32_t *sets, int64_t l,
+                         int64_t k, float *partials, int64_t lpad, hipStream_t st) {
+    constexpr int RPT = 4;
+    const int64_t G = (n + pl.rows - 1) / pl.rows;
+    const int64_t chunks = (l + pl.sets_per_chunk - 1) / pl.sets_per_chunk;
+    const size_t lds = ((size_t)pl.sets_per_chunk * k * pl.rec + 4 * (size_t)pl.sets_per_chunk) * sizeof(float);
+    hipLaunchKernelGGL((eval_valu_kernel<T, DP, RPT>), dim3((unsigned)G, (unsigned)chunks), dim3(256), lds, st,
+                       (const T *)V, n, d, sets, l, k, pl.sets_per_chunk, partials, lpad);
+    return hipGetLastError();
+}
+
+template <typename T>
+static hipError_t valu_dispatch(const ValuPlan &pl, const void *V, int64_t n, int d, const int32_t *sets, int64_t l,
+                                int64_t k, float *partials, int64_t lpad, hipStream_t st) {
+    switch (pl.dp) {
+    case 1: return valu_t<T, 1>(pl, V, n, d, sets, l, k, partials, lpad, st);
+    case 2: return valu_t<T, 2>(pl, V, n, d, sets, l, k, partials, lpad, st);
+    case 4: return valu_t<T, 4>(pl, V, n, d, sets, l, k, partials, lpad, st);
+    case 8: return valu_t<T, 8>(pl, V, n, d, sets, l, k, partials, lpad, st);
+    case 16: return valu_t<T, 16>(pl, V, n, d, sets, l, k, partials, lpad, st);
+    }
+    return hipErrorInvalidValue;
+}
+
+hipError_t launch_valu(int prec, const ValuPlan &pl, const void *V, int64_t n, int d, const int32_t *sets,
+                       int64_t l, int64_t k, float *partials, int64_t lpad, hipStream_t st) {
+    switch (prec) {
+    case P_FP32: return valu_dispatch<float>(pl, V, n, d, sets, l, k, partials, lpad, st);
+    case P_FP16: return valu_dispatch<_Float16>(pl, V, n, d, sets, l, k, partials, lpad, st);
+    case P_BF16: return valu_dispatch<__bf16>(pl, V, n, d, sets, l, k, partials, lpad, st);
+    }
+    return hipErrorInvalidValue;
+}
+
+// ---------------------------------------------------------------------------
+// Second pass: out[j] = (2/n) * sum_g partials[g][j].  Four fp64 running sums
+// over g = 0 mod 4, 1 mod 4, ... combined in a fixed tree, so the result does
+// not depend on how the partials were scheduled.  The index check turns a set
+// with an index outside [0, n) into NaN.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void reduce_partials_kernel(const float *__restrict__ partials, int64_t G,
+                                                              int64_t lpad, int64_t l, int64_t n,
+                                                              const int32_t *__restrict__ sets, int64_t kset,
+                                                              const int32_t *__restrict__ common, int64_t kcommon,
+                                                              float *__restrict__ out) {
+    const int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (j >= l) return;
+    double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
+    int64_t g = 0;
+    for (; g + 3 < G; g += 4) {
+        s0 += (double)partials[g * lpad + j];
+        s1 += (double)partials[(g + 1) * lpad + j];
+        s2 += (double)partials[(g + 2) * lpad + j];
+        s3 += (double)partials[(g + 3) * lpad + j];
+    }
+    if (g < G) s0 += (double)partials[g * lpad + j];
+    if (g + 1 < G) s1 += (double)partials[(g + 1) * lpad + j];
+    if (g + 2 < G) s2 += (double)partials[(g + 2) * lpad + j];
+    const double s = (s0 + s1) + (s2 + s3);
+    bool bad = false;
+    for (int64_t p = 0; p < kset; ++p) {
+        const int64_t idx = sets[j * kset + p];
+        bad |= idx < 0 || idx >= n;
+    }
+    for (int64_t p = 0; p < kcommon; ++p) {
+        const int64_t idx = common[p];
+        bad |= idx < 0 || idx >= n;
+    }
+    out[j] = bad ? __builtin_nanf("") : (float)(2.0 * s / (double)n);
+}
+
+hipError_t launch_reduce(const float *partials, int64_t G, int64_t lpad, int64_t l, int64_t n,
+                         const int32_t *sets, int64_t kset, const int32_t *common, int64_t kcommon, float *out,
+                         hipStream_t st) {
+    const int64_t blocks = (l + 255) / 256;
+    hipLaunchKernelGGL(reduce_partials_kernel, dim3((unsigned)blocks), dim3(256), 0, st, partials, G, lpad, l, n,
+                       sets, kset, common, kcommon, out);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// q[i] = ||v_i||^2 in fp32, coordinates in order (one thread per point).
+// ---------------------------------------------------------------------------
+template <typename T>
+__global__ __launch_bounds__(256) void sqnorm_kernel(const T *__restrict__ V, int64_t n, int d,
+                                                      float *__restrict__ q) {
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i >= n) return;
+    const T *row = V + i * (int64_t)d;
+    float s = 0.0f;
+    for (int t = 0; t < d; ++t) {
+        const float x = to_f32(row[t]);
+        s = fmaf(x, x, s);
+    }
+    q[i] = s;
+}
+
+hipError_t launch_sqnorm(int prec, const void *V, int64_t n, int d, float *q, hipStream_t st) {
+    const int64_t blocks = (n + 255) / 256;
+    switch (prec) {
+    case P_FP32:
+        hipLaunchKernelGGL(sqnorm_kernel<float>, dim3((unsigned)blocks), dim3(256), 0, st, (const float *)V, n, d, q);
+        break;
+    case P_FP16:
+        hipLaunchKernelGGL(sqnorm_kernel<_Float16>, dim3((unsigned)blocks), dim3(256), 0, st, (const _Float16 *)V, n,
+                           d, q);
+        break;
+    case P_BF16:
+        hipLaunchKernelGGL(sqnorm_kernel<__bf16>, dim3((unsigned)blocks), dim3(256), 0, st, (const __bf16 *)V, n, d,
+                           q);
+        break;
+    default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+}  // namespace exemcl

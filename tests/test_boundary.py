@@ -1,0 +1,120 @@
+"""The C-ABI library on the host: it loads, exports what include/exemcl.h
+declares, and rejects bad arguments before touching any device (CPU only)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2101_08763_amd import api
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "exemcl.h")
+FAKE = ctypes.c_void_p(0x1000)  # never dereferenced: validation fails or stops first
+
+
+def declared_symbols():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"EXEMCL_API\s+[^;(]*?\b(exemplar_\w+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return api.load()
+
+
+def test_header_declares_the_abi():
+    syms = declared_symbols()
+    assert set(api.EXPORTED) == set(syms), syms
+
+
+def test_library_exports_every_declared_symbol(lib):
+    for name in declared_symbols():
+        assert hasattr(lib, name), name
+    assert api.exemplar_version() >= 100
+
+
+def test_strerror(lib):
+    for status in range(4):
+        assert lib.exemplar_strerror(status)
+    assert lib.exemplar_strerror(99) == b"unknown status"
+
+
+BAD_EVAL = [
+    dict(V=None), dict(n=0), dict(n=-3), dict(n=2**31), dict(d=0), dict(d=-1),
+    dict(k=-1), dict(l=-1), dict(precision=3), dict(precision=-1),
+    dict(sets=None), dict(out=None),
+]
+
+
+@pytest.mark.parametrize("bad", BAD_EVAL, ids=[str(b) for b in BAD_EVAL])
+def test_eval_rejects(lib, bad):
+    a = dict(V=FAKE, n=100, d=8, sets=FAKE, l=4, k=3, precision=0, out=FAKE)
+    a.update(bad)
+    rc = lib.exemplar_eval(a["V"], a["n"], a["d"], a["sets"], a["l"], a["k"], a["precision"], a["out"], None)
+    assert rc == api.EXEMCL_EINVAL
+
+
+def test_eval_dimension_limit(lib):
+    rc = lib.exemplar_eval(FAKE, 100, 513, FAKE, 4, 3, 0, FAKE, None)
+    assert rc == api.EXEMCL_EINVAL
+    with pytest.raises(api.ExemclError):
+        api.exemplar_plan(100, 513, 4, 3)
+
+
+def test_eval_empty_batch_is_a_noop(lib):
+    assert lib.exemplar_eval(FAKE, 100, 8, None, 0, 3, 0, None, None) == api.EXEMCL_OK
+
+
+BAD_GAIN = [dict(V=None), dict(n=0), dict(d=0), dict(k=-1), dict(l=-1), dict(S=None), dict(cands=None),
+            dict(out=None)]
+
+
+@pytest.mark.parametrize("bad", BAD_GAIN, ids=[str(b) for b in BAD_GAIN])
+def test_gain_rejects(lib, bad):
+    a = dict(V=FAKE, n=100, d=8, S=FAKE, k=3, cands=FAKE, l=4, out=FAKE)
+    a.update(bad)
+    rc = lib.exemplar_gain(a["V"], a["n"], a["d"], a["S"], a["k"], a["cands"], a["l"], a["out"], None)
+    assert rc == api.EXEMCL_EINVAL
+
+
+def test_sqnorm_rejects(lib):
+    assert lib.exemplar_sqnorm(None, 10, 2, 0, FAKE, None) == api.EXEMCL_EINVAL
+    assert lib.exemplar_sqnorm(FAKE, 10, 2, 0, None, None) == api.EXEMCL_EINVAL
+    assert lib.exemplar_sqnorm(FAKE, 0, 2, 0, FAKE, None) == api.EXEMCL_EINVAL
+    assert lib.exemplar_sqnorm(FAKE, 10, 2, 7, FAKE, None) == api.EXEMCL_EINVAL
+
+
+def test_workspace_limit_gives_enomem(lib, monkeypatch):
+    """The chunking failure of Section IV-B: not even one batch fits."""
+    monkeypatch.setenv("EXEMCL_WORKSPACE_LIMIT", "1024")
+    rc = lib.exemplar_eval(FAKE, 100000, 32, FAKE, 256, 10, 0, FAKE, None)
+    assert rc == api.EXEMCL_ENOMEM
+    rc = lib.exemplar_gain(FAKE, 100000, 32, FAKE, 5, FAKE, 256, FAKE, None)
+    assert rc == api.EXEMCL_ENOMEM
+
+
+def test_plan_paths_depend_on_d_k_precision_only(monkeypatch):
+    monkeypatch.delenv("EXEMCL_PATH", raising=False)
+    for prec in (api.EXEMCL_FP32, api.EXEMCL_FP16, api.EXEMCL_BF16):
+        for d in (1, 2, 8, 16, 32, 100, 256, 512):
+            paths = {api.exemplar_plan(n, d, l, 10, prec)[0] for n in (1, 999, 10**6) for l in (1, 33, 4096)}
+            assert len(paths) == 1, (prec, d, paths)
+    assert api.exemplar_plan(10, 8, 0, 5)[0] == "none"
+    assert api.exemplar_plan(10, 8, 5, 0)[0] == "none"
+
+
+def test_plan_forced_paths(monkeypatch):
+    monkeypatch.setenv("EXEMCL_PATH", "valu")
+    assert api.exemplar_plan(1000, 8, 16, 5)[0] == "valu"
+    assert api.exemplar_plan(1000, 64, 16, 5)[0] == "mfma"  # beyond the VALU path's d
+    monkeypatch.setenv("EXEMCL_PATH", "mfma")
+    assert api.exemplar_plan(1000, 8, 16, 5)[0] == "mfma"
+
+
+def test_workspace_is_bounded():
+    """Temporary memory stays O(l*k*d + n*l/rows): the work matrix W of
+    Eq. (7) (l x n) is never materialised."""
+    path, ws = api.exemplar_plan(10**6, 256, 2048, 32, api.EXEMCL_FP16)
+    assert path == "mfma"
+    assert ws < 2048 * 10**6 * 4 / 20

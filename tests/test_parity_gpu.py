@@ -1,0 +1,295 @@
+"""GPU parity: the HIP library (through its C ABI) against the CPU fp64 oracle.
+
+Tolerance (|gpu - oracle| <= rtol*|oracle| + atol):
+  fp32 inputs:       rtol 1e-5, atol 1e-7 * L({e0})
+  fp16/bf16 inputs:  rtol 2e-2, atol 1e-4 * L({e0}), against the oracle run on
+                     the rounded values the GPU saw.
+The absolute floor is needed where f is near 0 (k = 0, e0-like exemplars).
+Index handling (which set is NaN, which result lands in which slot) is exact.
+"""
+import os
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2101_08763_amd import api, synth
+
+pytestmark = pytest.mark.gpu
+
+RTOL = {"fp32": 1e-5, "fp16": 2e-2, "bf16": 2e-2}
+ATOL = {"fp32": 1e-7, "fp16": 1e-4, "bf16": 1e-4}
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def torch_gpu():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    api.load()  # fails loudly when the library is missing
+    return torch
+
+
+@pytest.fixture(scope="module")
+def orc():
+    return oracle.load()
+
+
+@pytest.fixture(autouse=True)
+def _no_forced_path(monkeypatch):
+    monkeypatch.delenv("EXEMCL_PATH", raising=False)
+
+
+def to_gpu(torch, X, prec):
+    Xs, X64 = synth.rounded(X, prec)
+    t = Xs if isinstance(Xs, torch.Tensor) else torch.from_numpy(Xs)
+    return t.contiguous().cuda(), X64
+
+
+def gpu_eval(torch, Vg, sets):
+    s = torch.from_numpy(np.ascontiguousarray(sets, dtype=np.int32)).cuda()
+    out = api.exemplar_eval(Vg, s)
+    torch.cuda.synchronize()
+    return out.cpu().numpy().astype(np.float64)
+
+
+def check(got, want, le0, prec, what):
+    got = np.asarray(got, np.float64)
+    want = np.asarray(want, np.float64)
+    assert got.shape == want.shape
+    assert np.array_equal(np.isnan(got), np.isnan(want)), f"{what}: NaN pattern differs"
+    ok = ~np.isnan(want)
+    err = np.abs(got[ok] - want[ok])
+    bound = RTOL[prec] * np.abs(want[ok]) + ATOL[prec] * le0
+    worst = float(np.max(err / np.maximum(np.abs(want[ok]), 1e-300))) if ok.any() else 0.0
+    say(f"  {what}: {ok.sum()} values, max rel err {worst:.3e}")
+    assert np.all(err <= bound), f"{what}: max excess {(err - bound).max():.3e}"
+
+
+# ---------------------------------------------------------------------------
+# The tiny 1 000-point workload, on both paths.
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("path", ["mfma", "valu"])
+def test_tiny_workload(torch_gpu, orc, monkeypatch, path):
+    monkeypatch.setenv("EXEMCL_PATH", path)
+    p = synth.make("tiny")
+    say(f"tiny workload, path {path}")
+    Vg, X64 = to_gpu(torch_gpu, p.X, "fp32")
+    check(gpu_eval(torch_gpu, Vg, p.sets), orc.eval(X64, p.sets), orc.loss_e0(X64), "fp32", "tiny")
+
+
+# ---------------------------------------------------------------------------
+# Ragged sizes across tiles: n not a multiple of any row block, l spanning
+# several set groups with a partial last one, every d bucket incl. ragged d.
+# ---------------------------------------------------------------------------
+DIMS = [1, 2, 3, 5, 8, 13, 16, 17, 31, 32, 33, 64, 100, 127, 128, 200, 256, 300, 512]
+
+
+@pytest.mark.parametrize("prec", ["fp32", "fp16", "bf16"])
+@pytest.mark.parametrize("d", DIMS)
+def test_ragged_mfma(torch_gpu, orc, prec, d):
+    n, l, k = 1337, 70, 7
+    p = synth.random_problem(n, d, l, k, seed=1000 + d, clusters=4)
+    say(f"ragged mfma prec={prec} n={n} d={d} l={l} k={k}")
+    Vg, X64 = to_gpu(torch_gpu, p.X, prec)
+    check(gpu_eval(torch_gpu, Vg, p.sets), orc.eval(X64, p.sets, 8), orc.loss_e0(X64), prec, f"d={d}")
+
+
+@pytest.mark.parametrize("prec", ["fp32", "fp16", "bf16"])
+@pytest.mark.parametrize("d", [1, 2, 3, 8, 13, 16])
+def test_ragged_valu(torch_gpu, orc, monkeypatch, prec, d):
+    monkeypatch.setenv("EXEMCL_PATH", "valu")
+    n, l, k = 2500, 70, 9
+    p = synth.random_problem(n, d, l, k, seed=2000 + d)
+    say(f"ragged valu prec={prec} n={n} d={d}")
+    Vg, X64 = to_gpu(torch_gpu, p.X, prec)
+    check(gpu_eval(torch_gpu, Vg, p.sets), orc.eval(X64, p.sets, 8), orc.loss_e0(X64), prec, f"d={d}")
+
+
+@pytest.mark.parametrize("prec", ["fp16", "bf16"])
+def test_half_inputs_are_exact_in_fp32(torch_gpu, orc, prec):
+    """fp16/bf16 products are exact in fp32, so against the oracle on the
+    rounded inputs the error is fp32 accumulation only."""
+    p = synth.random_problem(3000, 64, 40, 11, seed=77, clusters=5)
+    Vg, X64 = to_gpu(torch_gpu, p.X, prec)
+    got = gpu_eval(torch_gpu, Vg, p.sets)
+    want = orc.eval(X64, p.sets, 8)
+    assert np.max(np.abs(got - want) / np.abs(want)) < 1e-5
+
+
+# ---------------------------------------------------------------------------
+# Full-size workloads (the benchmark's launch configuration) on all or on a
+# strided sample of sets.
+# ---------------------------------------------------------------------------
+def strided(l, m):
+    if l <= m:
+        return np.arange(l)
+    return np.unique((np.arange(m) * (l - 1)) // (m - 1))
+
+
+def test_mix50k_all_sets(torch_gpu, orc):
+    p = synth.make("mix50k")
+    say("mix50k: 50 000 x 32 fp32, 256 sets of 10")
+    Vg, X64 = to_gpu(torch_gpu, p.X, "fp32")
+    got = gpu_eval(torch_gpu, Vg, p.sets)
+    check(got, orc.eval(X64, p.sets, 0), orc.loss_e0(X64), "fp32", "mix50k")
+
+
+@pytest.mark.parametrize("d", [2, 16, 128, 512])
+@pytest.mark.parametrize("prec", ["fp32", "fp16"])
+def test_sweep_sampled(torch_gpu, orc, d, prec):
+    p = synth.make(f"sweep_d{d}_{prec}")
+    say(f"sweep d={d} {prec}: 100 000 points, 1024 sets of 16")
+    Vg, X64 = to_gpu(torch_gpu, p.X, prec)
+    got = gpu_eval(torch_gpu, Vg, p.sets)
+    idx = strided(len(p.sets), 16 if d >= 128 else 64)
+    check(got[idx], orc.eval(X64, p.sets[idx], 0), orc.loss_e0(X64), prec, f"sweep d={d}")
+    assert np.all(np.isfinite(got)) and np.all(got >= 0)
+
+
+def test_greedy200k_sampled(torch_gpu, orc):
+    p = synth.make("greedy200k")
+    say("greedy200k: 200 000 x 100 fp32, |S|=19, 4096 candidates")
+    Vg, X64 = to_gpu(torch_gpu, p.X, "fp32")
+    S = torch_gpu.from_numpy(p.S).cuda()
+    C = torch_gpu.from_numpy(p.cands).cuda()
+    got = api.exemplar_gain(Vg, S, C)
+    torch_gpu.cuda.synchronize()
+    got = got.cpu().numpy().astype(np.float64)
+    idx = strided(len(p.cands), 32)
+    check(got[idx], orc.gain(X64, p.S, p.cands[idx], 0), orc.loss_e0(X64), "fp32", "greedy200k")
+
+
+@pytest.mark.slow
+def test_large1m_sampled(torch_gpu, orc):
+    p = synth.make("large1m")
+    say("large1m: 1 000 000 x 256 fp16, 2048 sets of 32")
+    Vg, X64 = to_gpu(torch_gpu, p.X, "fp16")
+    got = gpu_eval(torch_gpu, Vg, p.sets)
+    idx = strided(len(p.sets), 4)
+    check(got[idx], orc.eval(X64, p.sets[idx], 0), orc.loss_e0(X64), "fp16", "large1m")
+    assert np.all(np.isfinite(got)) and np.all(got >= 0)
+
+
+# ---------------------------------------------------------------------------
+# Edge cases.
+# ---------------------------------------------------------------------------
+def test_edge_cases(torch_gpu, orc):
+    torch = torch_gpu
+    rng = np.random.default_rng(5)
+    X = rng.standard_normal((300, 5)).astype(np.float32)
+    Vg, X64 = to_gpu(torch, X, "fp32")
+    le0 = orc.loss_e0(X64)
+    # k = 0: f(empty) = 0 exactly
+    out = gpu_eval(torch, Vg, np.zeros((9, 0), np.int32))
+    assert np.all(out == 0.0)
+    # l = 0: nothing queued
+    e = api.exemplar_eval(Vg, torch.zeros((0, 3), dtype=torch.int32, device="cuda"))
+    assert e.numel() == 0
+    # invalid indices poison their own set only
+    sets = np.array([[1, 2, 3], [4, 300, 5], [-1, 0, 1], [7, 8, 9]], np.int32)
+    got = gpu_eval(torch, Vg, sets)
+    assert np.isnan(got[1]) and np.isnan(got[2]) and np.isfinite(got[[0, 3]]).all()
+    check(got, orc.eval(X64, sets), le0, "fp32", "invalid")
+    # duplicates and S = V
+    check(gpu_eval(torch, Vg, [[5, 5, 5, 6]]), orc.eval(X64, [[5, 6]]), le0, "fp32", "duplicates")
+    check(gpu_eval(torch, Vg, np.arange(300, dtype=np.int32)[None]), [le0], le0, "fp32", "S = V")
+    # n = 1: f({v}) = ||v||^2
+    one = torch.tensor([[3.0, -4.0]], device="cuda")
+    assert abs(gpu_eval(torch, one, [[0]])[0] - 25.0) <= 25.0 * 1e-6
+    line = np.array([[1.0], [2.0], [3.0]], np.float32)
+    Lg, _ = to_gpu(torch, line, "fp32")
+    check(gpu_eval(torch, Lg, [[0], [1], [2], [0, 1]]), [3.0, 4.0, 4.0, 13 / 3], 14 / 3, "fp32", "worked example")
+
+
+def test_sqnorm(torch_gpu, orc):
+    for prec in ("fp32", "fp16", "bf16"):
+        p = synth.random_problem(5000, 37, 1, 1, seed=3, clusters=3)
+        Vg, X64 = to_gpu(torch_gpu, p.X, prec)
+        q = api.exemplar_sqnorm(Vg)
+        torch_gpu.cuda.synchronize()
+        want = orc.sqnorm(X64)
+        np.testing.assert_allclose(q.cpu().numpy(), want, rtol=1e-5, atol=0)
+
+
+# ---------------------------------------------------------------------------
+# Greedy scoring.
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("d", [3, 32, 100, 300])
+def test_gain_matches_direct(torch_gpu, orc, d):
+    torch = torch_gpu
+    p = synth.random_problem(2100, d, 1, 1, seed=40 + d, clusters=6)
+    rng = np.random.default_rng(d)
+    S = rng.choice(2100, 45, replace=False).astype(np.int32)
+    cands = np.concatenate([rng.choice(2100, 90, replace=False), S[:3], [2099, 0]]).astype(np.int32)
+    Vg, X64 = to_gpu(torch, p.X, "fp32")
+    got = api.exemplar_gain(Vg, torch.from_numpy(S).cuda(), torch.from_numpy(cands).cuda())
+    torch.cuda.synchronize()
+    got = got.cpu().numpy().astype(np.float64)
+    le0 = orc.loss_e0(X64)
+    check(got, orc.gain(X64, S, cands, 8), le0, "fp32", f"gain d={d}")
+    fS = orc.eval(X64, S[None])[0]
+    check(got[90:93], [fS] * 3, le0, "fp32", "candidate in S")
+    # against exemplar_eval on S u {c}
+    sets = np.concatenate([np.tile(S, (len(cands), 1)), cands[:, None]], axis=1)
+    check(got, gpu_eval(torch, Vg, sets), le0, "fp32", "gain vs eval")
+
+
+def test_gain_empty_base_and_invalid(torch_gpu, orc):
+    torch = torch_gpu
+    p = synth.random_problem(700, 9, 1, 1, seed=9)
+    Vg, X64 = to_gpu(torch, p.X, "fp32")
+    c = np.array([0, 5, 699, 700, -2], np.int32)
+    got = api.exemplar_gain(Vg, torch.zeros(0, dtype=torch.int32, device="cuda"), torch.from_numpy(c).cuda())
+    torch.cuda.synchronize()
+    got = got.cpu().numpy()
+    assert np.isnan(got[3]) and np.isnan(got[4])
+    check(got[:3], orc.eval(X64, c[:3, None]), orc.loss_e0(X64), "fp32", "empty base")
+    bad_S = torch.tensor([1, 9999], dtype=torch.int32, device="cuda")
+    got = api.exemplar_gain(Vg, bad_S, torch.from_numpy(c[:3]).cuda())
+    torch.cuda.synchronize()
+    assert np.isnan(got.cpu().numpy()).all()
+
+
+# ---------------------------------------------------------------------------
+# Determinism and batch independence (bitwise).
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("prec", ["fp32", "fp16"])
+def test_batch_independence_bitwise(torch_gpu, prec):
+    torch = torch_gpu
+    p = synth.random_problem(4000, 48, 100, 8, seed=21, clusters=3)
+    Vg, _ = to_gpu(torch, p.X, prec)
+    a = gpu_eval(torch, Vg, p.sets)
+    assert np.array_equal(a, gpu_eval(torch, Vg, p.sets)), "repeat"
+    perm = np.random.default_rng(0).permutation(100)
+    assert np.array_equal(a[perm], gpu_eval(torch, Vg, p.sets[perm])), "batch position"
+    assert np.array_equal(a[37:38], gpu_eval(torch, Vg, p.sets[37:38])), "batch size 1"
+    assert np.array_equal(a[:33], gpu_eval(torch, Vg, p.sets[:33])), "batch size 33"
+    slots = p.sets[:, ::-1].copy()
+    assert np.array_equal(a, gpu_eval(torch, Vg, slots)), "member order"
+
+
+def test_scaling_by_two_is_exact(torch_gpu):
+    torch = torch_gpu
+    p = synth.random_problem(3000, 20, 50, 6, seed=22)
+    Vg, _ = to_gpu(torch, p.X, "fp32")
+    a = gpu_eval(torch, Vg, p.sets)
+    b = gpu_eval(torch, (2.0 * Vg).contiguous(), p.sets)
+    assert np.array_equal(b, 4.0 * a)
+
+
+def test_paths_agree(torch_gpu, orc, monkeypatch):
+    torch = torch_gpu
+    p = synth.random_problem(6000, 16, 64, 12, seed=23, clusters=2)
+    Vg, X64 = to_gpu(torch, p.X, "fp32")
+    monkeypatch.setenv("EXEMCL_PATH", "valu")
+    a = gpu_eval(torch, Vg, p.sets)
+    monkeypatch.setenv("EXEMCL_PATH", "mfma")
+    b = gpu_eval(torch, Vg, p.sets)
+    check(a, b, orc.loss_e0(X64), "fp32", "valu vs mfma")
