@@ -20,15 +20,22 @@ LIB = os.path.join(PKG, "libexemcl.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
-SOURCES = ["host.cpp", "kernels_mfma.hip", "kernels_aux.hip"]
+SOURCES = ["host.cpp", "kernels_mfma.hip", "kernels_mfma_f32.hip", "kernels_mfma_f16.hip",
+           "kernels_mfma_bf16.hip", "kernels_aux.hip"]
 FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-fvisibility=hidden",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
          "-Wall", "-Wno-unused-result", f"-I{INCLUDE}", f"-I{CSRC}"]
 
 
+# The matrix-core kernels: accumulators in VGPRs (the epilogue reads them
+# directly), and max without NaN canonicalisation (inputs are finite).
+MFMA_FLAGS = ["-mllvm", "-amdgpu-mfma-vgpr-form", "-fno-honor-nans"]
+
+
 def _compile(src: str, verbose: bool) -> str:
     obj = os.path.join(OBJDIR, os.path.splitext(src)[0] + ".o")
-    cmd = [HIPCC, *FLAGS, "-x", "hip", "-c", os.path.join(CSRC, src), "-o", obj]
+    extra = MFMA_FLAGS if src.startswith("kernels_mfma_") else []
+    cmd = [HIPCC, *FLAGS, *extra, "-x", "hip", "-c", os.path.join(CSRC, src), "-o", obj]
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)

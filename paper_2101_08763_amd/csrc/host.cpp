@@ -59,10 +59,10 @@ struct Layout {
     MfmaPlan mp{};
     ValuPlan vp{};
     int64_t G = 0, lpad = 0, ngroups = 0, gpc = 0;
-    int64_t off_partials = 0, off_tiles = 0, off_bias = 0, off_aux = 0, bytes = 0;
+    int64_t off_partials = 0, off_tiles = 0, off_aux = 0, bytes = 0;
 };
 
-int64_t tile_bytes(const MfmaPlan &mp) { return (int64_t)mp.nkb * 64 * 16; }
+int64_t tile_bytes(const MfmaPlan &mp) { return mfma_tile_bytes(mp); }
 
 // Workspace of one exemplar_eval call (or of the scoring half of a gain call).
 bool layout_eval(int64_t n, int64_t d, int64_t l, int64_t k, int precision, int path, Layout *L) {
@@ -72,18 +72,18 @@ bool layout_eval(int64_t n, int64_t d, int64_t l, int64_t k, int precision, int 
         const int64_t tm = L->mp.tile;
         L->ngroups = (l + tm - 1) / tm;
         L->lpad = L->ngroups * tm;
-        L->G = (n + L->mp.rows - 1) / L->mp.rows;
+        const int64_t nrb = (n + L->mp.rows - 1) / L->mp.rows;
+        L->G = nrb * L->mp.waves;  // one partial-sum row per wavefront
         // Enough workgroups to cover 256 CUs several times; a chunk of set
         // groups shares one load of the workgroup's points.
-        int64_t chunks = (2048 + L->G - 1) / L->G;
+        int64_t chunks = (2048 + nrb - 1) / nrb;
         if (chunks < 1) chunks = 1;
         if (chunks > L->ngroups) chunks = L->ngroups;
         if (chunks > 65535) chunks = 65535;
         L->gpc = (L->ngroups + chunks - 1) / chunks;
         L->off_partials = 0;
         L->off_tiles = align_up(L->G * L->lpad * 4, 256);
-        L->off_bias = align_up(L->off_tiles + L->ngroups * k * tile_bytes(L->mp), 256);
-        L->off_aux = align_up(L->off_bias + L->ngroups * k * tm * 4, 256);
+        L->off_aux = align_up(L->off_tiles + L->ngroups * k * tile_bytes(L->mp), 256);
         L->bytes = L->off_aux;
         return true;
     }
@@ -219,11 +219,10 @@ int run_eval(const void *V, int64_t n, int64_t d, const int32_t *sets, int64_t l
     hipError_t e = hipSuccess;
     if (path == EXEMCL_PATH_MFMA) {
         void *tiles = base + L.off_tiles;
-        float *bias = (float *)(base + L.off_bias);
-        e = launch_pack(precision, L.mp, V, n, (int)d, sets, l, k, tiles, bias, st);
+        e = launch_pack(precision, L.mp, V, n, (int)d, sets, l, k, tiles, st);
         if (e == hipSuccess) {
             ProfRange pr(st);
-            e = launch_mfma(precision, MODE_SUM, L.mp, V, n, (int)d, tiles, bias, k, L.ngroups, L.gpc, m0, partials,
+            e = launch_mfma(precision, MODE_SUM, L.mp, V, n, (int)d, tiles, k, L.ngroups, L.gpc, m0, partials,
                             L.lpad, nullptr, st);
             pr.end();
         }
@@ -267,19 +266,17 @@ EXEMCL_API int exemplar_gain(const float *V, int64_t n, int64_t d, const int32_t
     const int64_t tm = mp.tile;
     const int64_t ngroups = (k + tm - 1) / tm;
     const int64_t off_tiles = align_up(n * 4, 256);
-    const int64_t off_bias = align_up(off_tiles + ngroups * tile_bytes(mp), 256);
-    const int64_t bytes = align_up(off_bias + ngroups * tm * 4, 256);
+    const int64_t bytes = align_up(off_tiles + ngroups * tile_bytes(mp), 256);
     Scratch ws;
     rc = alloc_scratch(&ws, bytes, st);
     if (rc) return rc;
     char *base = (char *)ws.ptr;
     float *gcache = (float *)base;
     void *tiles = base + off_tiles;
-    float *bias = (float *)(base + off_bias);
-    hipError_t e = launch_pack(EXEMCL_FP32, mp, V, n, (int)d, S, k, 1, tiles, bias, st);
+    hipError_t e = launch_pack(EXEMCL_FP32, mp, V, n, (int)d, S, k, 1, tiles, st);
     if (e == hipSuccess)
-        e = launch_mfma(EXEMCL_FP32, MODE_ROWMAX, mp, V, n, (int)d, tiles, bias, 1, ngroups, ngroups, nullptr,
-                        nullptr, 0, gcache, st);
+        e = launch_mfma(EXEMCL_FP32, MODE_ROWMAX, mp, V, n, (int)d, tiles, 1, ngroups, ngroups, nullptr, nullptr, 0,
+                        gcache, st);
     if (e != hipSuccess) return EXEMCL_EDEVICE;
     // Score every S u {c}: single-member sets {c} with the running max
     // started at g(v) instead of e0's 0.

@@ -14,9 +14,8 @@ enum Prec { P_FP32 = 0, P_FP16 = 1, P_BF16 = 2 };
 // depend on the batch it arrives in.
 struct MfmaPlan {
     int tile;       // TM: sets per column tile (32 or 16)
-    int kbmax;      // compile-time k-block capacity of the kernel
-    int nkb;        // k-blocks actually used, ceil(d / kb_dims)
-    int nks;        // MFMA instructions per tile, ceil(d / kstep)
+    int nkb;        // k-blocks per tile: ceil(d / kb_dims) rounded up to a compiled bucket
+    int nks_last;   // MFMA instructions fed by the last k-block
     int rt;         // row tiles per wavefront
     int waves;      // wavefronts per workgroup
     int rows;       // rows per workgroup = waves * rt * tile
@@ -24,6 +23,30 @@ struct MfmaPlan {
 };
 
 bool mfma_plan(int prec, int64_t d, MfmaPlan *p);
+
+// Arguments of one launch of the MFMA evaluation kernel.
+struct MfmaArgs {
+    const void *V;
+    int64_t n;
+    int d;
+    const void *tiles;
+    int64_t k, ngroups, gpc;
+    const float *m0;
+    float *partials;
+    int64_t lpad;
+    float *rowmax;
+};
+
+// Per-storage-type instantiations (kernels_mfma_{f32,f16,bf16}.hip).
+hipError_t pack_run_f32(const MfmaPlan &pl, const void *V, int64_t n, int d, const int32_t *sets, int64_t l,
+                        int64_t k, void *tiles, hipStream_t st);
+hipError_t pack_run_f16(const MfmaPlan &pl, const void *V, int64_t n, int d, const int32_t *sets, int64_t l,
+                        int64_t k, void *tiles, hipStream_t st);
+hipError_t pack_run_bf16(const MfmaPlan &pl, const void *V, int64_t n, int d, const int32_t *sets, int64_t l,
+                         int64_t k, void *tiles, hipStream_t st);
+hipError_t eval_run_f32(const MfmaPlan &pl, int mode, const MfmaArgs &x, hipStream_t st);
+hipError_t eval_run_f16(const MfmaPlan &pl, int mode, const MfmaArgs &x, hipStream_t st);
+hipError_t eval_run_bf16(const MfmaPlan &pl, int mode, const MfmaArgs &x, hipStream_t st);
 
 // Geometry of one VALU evaluation launch.
 struct ValuPlan {
@@ -37,19 +60,23 @@ struct ValuPlan {
 bool valu_plan(int prec, int64_t d, int64_t k, ValuPlan *p);
 
 // Stage the exemplar tiles of `l` sets of `k` indices: for every (set group,
-// slot) pair one TM-column tile of B lane vectors and one TM-vector of
-// biases -||s||^2/2 (-FLT_MAX for padding columns and invalid indices).
+// slot) pair one TM-column tile holding TM biases -||s||^2/2 (-FLT_MAX for
+// padding columns and invalid indices) and the B lane vectors.
 hipError_t launch_pack(int prec, const MfmaPlan &pl, const void *V, int64_t n, int d, const int32_t *sets,
-                       int64_t l, int64_t k, void *tiles, float *bias, hipStream_t st);
+                       int64_t l, int64_t k, void *tiles, hipStream_t st);
+
+// Bytes of one staged tile (bias header + B lane vectors).
+int64_t mfma_tile_bytes(const MfmaPlan &pl);
 
 // Mode of the MFMA kernel's epilogue.
 enum Mode { MODE_SUM = 0, MODE_ROWMAX = 1 };
 
-// partials[rb * lpad + j] = sum over the rows of block rb of
-// max(m0(v), max_p (<v, s_jp> - ||s_jp||^2 / 2)); m0 = 0 when null.
-// MODE_ROWMAX instead writes rowmax[v] = max(0, max over all staged columns).
+// partials[(rb * waves + w) * lpad + j] = sum over the rows of wavefront w
+// of row block rb of max(m0(v), max_p (<v, s_jp> - ||s_jp||^2 / 2)); m0 = 0
+// when null.  MODE_ROWMAX instead writes rowmax[v] = max(0, max over all
+// staged columns).
 hipError_t launch_mfma(int prec, int mode, const MfmaPlan &pl, const void *V, int64_t n, int d,
-                       const void *tiles, const float *bias, int64_t k, int64_t ngroups, int64_t groups_per_chunk,
+                       const void *tiles, int64_t k, int64_t ngroups, int64_t groups_per_chunk,
                        const float *m0, float *partials, int64_t lpad, float *rowmax, hipStream_t st);
 
 hipError_t launch_valu(int prec, const ValuPlan &pl, const void *V, int64_t n, int d, const int32_t *sets,

@@ -1,0 +1,17 @@
+// kernels_mfma_f16.hip -- fp16 instantiations of the MFMA kernels
+// (v_mfma_f32_32x32x16_f16, fp32 accumulate).
+#include "mfma_kernels.hpp"
+
+namespace exemcl {
+
+hipError_t pack_run_f16(const MfmaPlan &pl, const void *V, int64_t n, int d, const int32_t *sets, int64_t l,
+                        int64_t k, void *tiles, hipStream_t st) {
+    return pack_launch<_Float16, 32>(pl, V, n, d, sets, l, k, tiles, st);
+}
+
+hipError_t eval_run_f16(const MfmaPlan &pl, int mode, const MfmaArgs &x, hipStream_t st) {
+    (void)mode;
+    return eval_dispatch<_Float16, 32, MODE_SUM>(pl, x, st);
+}
+
+}  // namespace exemcl

@@ -1,0 +1,406 @@
+// mfma_kernels.hpp -- exemplar staging and the matrix-core evaluation kernel
+// (templates; instantiated per storage type in kernels_mfma_*.hip).
+//
+// The paper's GPU algorithm (Algorithm 3) assigns one thread to each cell
+// W[j][i] = min_{s in S_j} d(v_i, s) / n of the work matrix (Eq. (7)), loops
+// over the set members and writes W to global memory before a row sum
+// (Section IV-B).  Here the same quantity is computed as a dense contraction
+// on the MFMA units with a fused epilogue, and W is never materialised:
+//
+//   min(||v||^2, min_s ||v - s||^2) = ||v||^2 - 2 max(0, max_s h_s(v)),
+//   h_s(v) = <v, s> - ||s||^2 / 2,
+//
+// so f(S) = L({e0}) - L(S u {e0}) = (2/n) sum_v max(0, max_s h_s(v)).  The 0
+// is e0's contribution (Eq. (4)).  For every (row block, wavefront, set) a
+// partial sum is written; a second pass adds the partials in a fixed order.
+//
+// Data layout.  A workgroup owns WAVES*RT*TM consecutive ground points and
+// keeps them in registers in MFMA A-operand order for its whole life.
+// Exemplars are streamed: for every (group of TM sets, member p) a "tile"
+// holds the p-th member of each of the TM sets, already in B-operand order,
+// plus one fp32 bias -||s||^2/2 per column.  Tiles stream through a ring of
+// LDS stage buffers.  Each lane's output column is one set, so the minimum
+// over a set's members is a per-register running max across successive tiles
+// -- no cross-lane traffic until the set group ends.
+//
+// The number of k-blocks NKB is a compile-time bucket (d is zero-padded up to
+// it), so every MFMA chain is straight-line code: a runtime bound on the
+// k-loop would split the chain into basic blocks, and the accumulators would
+// be copied out of and back into the matrix-core registers at every split.
+#pragma once
+
+#include <float.h>
+
+#include "device.hpp"
+#include "internal.h"
+
+namespace exemcl {
+
+constexpr int HDR = 128;  // tile header: TM fp32 biases, padded to 128 bytes
+
+template <int NKB>
+constexpr int tile_bytes_of() {
+    return HDR + NKB * 1024;
+}
+
+// ---------------------------------------------------------------------------
+// Staging: gather exemplar rows by index into tiles, with their norms.
+//
+// Tile t = g*k + p holds, for the TM sets g*TM .. g*TM+TM-1, their member p.
+// Byte layout of one tile (HDR + nkb * 1024 bytes):
+//   [0, HDR)               TM fp32 biases -||s||^2/2, one per column
+//   [HDR + kb*1024 + 16*L)  lane L's 16-byte B-operand vector for k-block kb
+// Padding columns (set >= l) and invalid indices become zero vectors with
+// bias -FLT_MAX, which never wins the running max.  Coordinates past d are
+// zero.  One wavefront per tile.
+// ---------------------------------------------------------------------------
+template <typename T, int TILE>
+__global__ __launch_bounds__(64) void pack_tiles_kernel(const T *__restrict__ V, int64_t n, int d,
+                                                        const int32_t *__restrict__ sets, int64_t l,
+                                                        int64_t k, int nkb, unsigned char *__restrict__ tiles,
+                                                        bool vec_ok) {
+    using M = Mfma<T, TILE>;
+    const int64_t t = blockIdx.x;
+    const int64_t g = t / k, p = t - (t / k) * k;
+    const int lane = threadIdx.x;
+    const int col = lane % M::TM, grp = lane / M::TM;
+    const int64_t j = g * M::TM + col;
+    int64_t idx = -1;
+    if (j < l) idx = sets[j * k + p];
+    const bool valid = idx >= 0 && idx < n;
+    unsigned char *tile = tiles + t * (int64_t)(HDR + nkb * 1024);
+    typename M::vec_t *dst = reinterpret_cast<typename M::vec_t *>(tile + HDR);
+    for (int kb = 0; kb < nkb; ++kb) {
+        dst[kb * 64 + lane] = load_lanevec<M>(V, n, d, valid ? idx : n, kb, grp, vec_ok);
+    }
+    if (grp == 0) {
+        float q = 0.0f;
+        if (valid) {
+            const T *row = V + idx * (int64_t)d;
+            for (int e = 0; e < d; ++e) {
+                const float x = to_f32(row[e]);
+                q = fmaf(x, x, q);
+            }
+        }
+        reinterpret_cast<float *>(tile)[col] = valid ? -0.5f * q : -FLT_MAX;
+    }
+}
+
+// Bytes of one LDS stage buffer: at least 16 KiB and one whole tile, a
+// multiple of one 16-byte load per thread.
+template <int NKB, int WAVES>
+constexpr int stage_bytes() {
+    constexpr int per_round = WAVES * 64 * 16;
+    constexpr int tb = tile_bytes_of<NKB>();
+    constexpr int need = tb > 16384 ? tb : 16384;
+    return (need + per_round - 1) / per_round * per_round;
+}
+
+template <int NKB>
+constexpr int ring_depth() {
+    return 3;
+}
+
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+// ---------------------------------------------------------------------------
+// Evaluation kernel.
+//
+// grid.x = row blocks of WAVES*RT*TM consecutive points, grid.y = chunks of
+// gpc set groups.  Wavefront w owns RT row tiles of TM points.
+//
+// The chunk's tiles are one contiguous byte range in global memory, streamed
+// into a ring of NBUF LDS stage buffers of SB bytes (TPS whole tiles each) by
+// direct global->LDS loads (global_load_lds_dwordx4).  Every thread issues
+// exactly CNT 16-byte loads per stage, so "stage s has landed while the next
+// NBUF-2 stages are in flight" is vmcnt(CNT*(NBUF-2)).  One barrier per stage
+// both publishes stage s and frees the buffer of stage s-1 for stage
+// s+NBUF-1.
+//
+// NKS_LAST = MFMA instructions fed by the last k-block (fp32 packs KS_PER_KB
+// instructions per k-block; tiny d uses fewer).
+//
+// MODE_SUM: each wavefront writes its partial sum per set,
+//   partials[(rb * WAVES + w) * lpad + j] = sum over its rows of
+//   max(m0(v), max_p h_{s_jp}(v)),
+// in a fixed order (its registers, then the K-groups of the MFMA layout).
+// MODE_ROWMAX: rowmax[v] = max(0, max over all staged columns of h_s(v)).
+// ---------------------------------------------------------------------------
+template <typename T, int TILE, int NKB, int NKS_LAST, int RT, int WAVES, int MODE, bool HAS_M0>
+__global__ __launch_bounds__(WAVES * 64) void eval_mfma_kernel(const T *__restrict__ V, int64_t n, int d,
+                                                                 const unsigned char *__restrict__ tiles, int64_t k,
+                                                                 int64_t ngroups, int64_t gpc,
+                                                                 const float *__restrict__ m0,
+                                                                 float *__restrict__ partials, int64_t lpad,
+                                                                 float *__restrict__ rowmax, bool vec_ok) {
+    using M = Mfma<T, TILE>;
+    using vec_t = typename M::vec_t;
+    using acc_t = typename M::acc_t;
+    constexpr int TM = M::TM;
+    constexpr int NT = WAVES * 64;
+    constexpr int TB = tile_bytes_of<NKB>();
+    constexpr int SB = stage_bytes<NKB, WAVES>();
+    constexpr int TPS = SB / TB;
+    constexpr int CNT = SB / (NT * 16);
+    constexpr int NBUF = ring_depth<NKB>();
+    constexpr int PF = NKB < 3 ? NKB : 3;  // B fragments in flight ahead of use
+    static_assert(TPS >= 1 && NBUF >= 2, "stage geometry");
+    static_assert(NKS_LAST >= 1 && NKS_LAST <= M::KS_PER_KB, "k-steps of the last block");
+
+    extern __shared__ __align__(16) unsigned char smem[];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63, wave = tid >> 6;
+    const int lr = lane % TM, grp = lane / TM;
+    const int64_t rb = blockIdx.x;
+    const int64_t g0 = (int64_t)blockIdx.y * gpc;
+    const int64_t g1 = min(ngroups, g0 + gpc);
+    const int64_t row0 = rb * (int64_t)(WAVES * RT * TM) + (int64_t)wave * RT * TM;
+
+    const int64_t ntiles = (g1 - g0) * k;
+    const int64_t nstages = (ntiles + TPS - 1) / TPS;
+    const unsigned char *chunk = tiles + g0 * k * (int64_t)TB;
+    const int64_t chunk_bytes = ntiles * (int64_t)TB;
+
+    // Queue the direct-to-LDS copy of stage s (CNT loads per thread; loads past
+    // the chunk end re-read its first bytes into unused buffer space).
+    auto issue = [&](int64_t s) {
+        unsigned char *buf = smem + (int)(s % NBUF) * SB;
+        const int64_t base = s * (int64_t)(TPS * TB);
+        const int64_t end = min(chunk_bytes, base + (int64_t)(TPS * TB));
+#pragma unroll
+        for (int r = 0; r < CNT; ++r) {
+            const int64_t off = base + (int64_t)(r * NT + tid) * 16;
+            const unsigned char *src = off < end ? chunk + off : chunk;
+            __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void *)src,
+                                             (__attribute__((address_space(3))) void *)(buf + (r * NT + wave * 64) * 16),
+                                             16, 0, 0);
+        }
+    };
+
+    if (nstages > 0) {
+#pragma unroll
+        for (int s = 0; s < NBUF - 1; ++s)
+            if (s < nstages) issue(s);
+    }
+
+    // Ground points of this wavefront, in A-operand order, resident for the
+    // whole kernel (zero past d and past n).
+    vec_t a[RT][NKB];
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+        for (int kb = 0; kb < NKB; ++kb) a[rt][kb] = load_lanevec<M>(V, n, d, row0 + rt * TM + lr, kb, grp, vec_ok);
+
+    // Initial value of the running max for each output element: e0's 0, or
+    // (HAS_M0) the per-point cached value when scoring S u {c}.
+    float minit[HAS_M0 ? RT : 1][HAS_M0 ? M::ACC : 1];
+    if constexpr (HAS_M0) {
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+            for (int i = 0; i < M::ACC; ++i) {
+                const int64_t r = row0 + rt * TM + out_row<TM>(i, grp);
+                minit[rt][i] = r < n ? m0[r] : 0.0f;
+            }
+    }
+    auto m_init = [&](int rt, int i) -> float {
+        if constexpr (HAS_M0) return minit[rt][i];
+        else return 0.0f;
+    };
+    float m[RT][M::ACC];
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+        for (int i = 0; i < M::ACC; ++i) m[rt][i] = m_init(rt, i);
+
+    float *wpart = partials + (rb * WAVES + wave) * lpad;
+    int64_t g = g0;
+    int64_t p = 0;
+    for (int64_t s = 0; s < nstages; ++s) {
+        if (s + NBUF - 2 < nstages) wait_vmcnt<CNT * (NBUF - 2)>();
+        else wait_vmcnt<0>();
+        __syncthreads();
+        if (s + NBUF - 1 < nstages) issue(s + NBUF - 1);
+
+        const unsigned char *buf = smem + (int)(s % NBUF) * SB;
+        const int tn = (int)min((int64_t)TPS, ntiles - s * TPS);
+        for (int tt = 0; tt < tn; ++tt) {
+            const unsigned char *tb = buf + tt * TB;
+            const vec_t *B = reinterpret_cast<const vec_t *>(tb + HDR);
+            vec_t bq[PF];
+#pragma unroll
+            for (int i = 0; i < PF; ++i) bq[i] = B[i * 64 + lane];
+            const float b = reinterpret_cast<const float *>(tb)[lr];
+
+            // The bias enters as the accumulator's initial value, in fp32.
+            acc_t acc[RT];
+#pragma unroll
+            for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+                for (int i = 0; i < M::ACC; ++i) acc[rt][i] = b;
+#pragma unroll
+            for (int kb = 0; kb < NKB; ++kb) {
+                const vec_t bv = bq[kb % PF];
+                if (kb + PF < NKB) bq[kb % PF] = B[(kb + PF) * 64 + lane];
+#pragma unroll
+                for (int e = 0; e < M::KS_PER_KB; ++e) {
+                    if (kb < NKB - 1 || e < NKS_LAST) {
+#pragma unroll
+                        for (int rt = 0; rt < RT; ++rt) acc[rt] = M::mma(a[rt][kb], bv, e, acc[rt]);
+                    }
+                }
+            }
+#pragma unroll
+            for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+                for (int i = 0; i < M::ACC; ++i) m[rt][i] = fmaxf(m[rt][i], acc[rt][i]);
+
+            if constexpr (MODE == MODE_SUM) {
+                if (p == k - 1) {
+                    // Sum this lane's rows for its column, then the K-groups
+                    // holding the other rows of the same column.
+                    float sum = 0.0f;
+#pragma unroll
+                    for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+                        for (int i = 0; i < M::ACC; ++i) sum += m[rt][i];
+#pragma unroll
+                    for (int off = TM; off < 64; off <<= 1) sum += __shfl_xor(sum, off);
+                    if (grp == 0) wpart[g * TM + lr] = sum;
+#pragma unroll
+                    for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+                        for (int i = 0; i < M::ACC; ++i) m[rt][i] = m_init(rt, i);
+                }
+            }
+            if (++p == k) {
+                p = 0;
+                ++g;
+            }
+        }
+    }
+
+    if constexpr (MODE == MODE_ROWMAX) {
+        // Maximum over all staged columns (the members of S) for every row,
+        // clamped at e0's 0: the per-point cache g(v).
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+            for (int i = 0; i < M::ACC; ++i) {
+                float x = fmaxf(m[rt][i], 0.0f);
+#pragma unroll
+                for (int off = 1; off < TM; off <<= 1) x = fmaxf(x, __shfl_xor(x, off));
+                m[rt][i] = x;
+            }
+        if (lr == 0) {
+#pragma unroll
+            for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+                for (int i = 0; i < M::ACC; ++i) {
+                    const int64_t r = row0 + rt * TM + out_row<TM>(i, grp);
+                    if (r < n) rowmax[r] = m[rt][i];
+                }
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Host-side launch helpers.
+// ---------------------------------------------------------------------------
+template <typename T, int TILE>
+hipError_t pack_launch(const MfmaPlan &pl, const void *V, int64_t n, int d, const int32_t *sets, int64_t l,
+                       int64_t k, void *tiles, hipStream_t st) {
+    const int64_t ngroups = (l + TILE - 1) / TILE;
+    const bool vec_ok = ((uintptr_t)V % 16 == 0) && ((d * (int64_t)sizeof(T)) % 16 == 0);
+    hipLaunchKernelGGL((pack_tiles_kernel<T, TILE>), dim3((unsigned)(ngroups * k)), dim3(64), 0, st,
+                       (const T *)V, n, d, sets, l, k, pl.nkb, (unsigned char *)tiles, vec_ok);
+    return hipGetLastError();
+}
+
+template <typename T, int TILE, int NKB, int NKS_LAST, int RT, int WAVES, int MODE, bool HAS_M0>
+hipError_t eval_launch_t(const MfmaArgs &x, hipStream_t st) {
+    constexpr int SB = stage_bytes<NKB, WAVES>();
+    constexpr int NBUF = ring_depth<NKB>();
+    auto kern = eval_mfma_kernel<T, TILE, NKB, NKS_LAST, RT, WAVES, MODE, HAS_M0>;
+    const size_t lds = (size_t)NBUF * SB;
+    if (lds > 64 * 1024) {
+        hipError_t e = hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        if (e != hipSuccess) return e;
+    }
+    const int64_t rows = (int64_t)WAVES * RT * TILE;
+    const int64_t G = (x.n + rows - 1) / rows;
+    const int64_t chunks = (x.ngroups + x.gpc - 1) / x.gpc;
+    const bool vec_ok = ((uintptr_t)x.V % 16 == 0) && ((x.d * (int64_t)sizeof(T)) % 16 == 0);
+    hipLaunchKernelGGL(kern, dim3((unsigned)G, (unsigned)chunks), dim3(WAVES * 64), lds, st, (const T *)x.V, x.n,
+                       x.d, (const unsigned char *)x.tiles, x.k, x.ngroups, x.gpc, x.m0, x.partials, x.lpad,
+                       x.rowmax, vec_ok);
+    return hipGetLastError();
+}
+
+template <typename T, int TILE, int NKB, int NKS_LAST, int RT, int WAVES, int MODE>
+hipError_t eval_launch(const MfmaArgs &x, hipStream_t st) {
+    if constexpr (MODE == MODE_SUM && sizeof(T) == 4) {
+        if (x.m0) return eval_launch_t<T, TILE, NKB, NKS_LAST, RT, WAVES, MODE, true>(x, st);
+    }
+    return eval_launch_t<T, TILE, NKB, NKS_LAST, RT, WAVES, MODE, false>(x, st);
+}
+
+// Wavefronts per workgroup for a k-block bucket (the plan uses the same rule).
+template <int NKB>
+constexpr int waves_for() {
+    return NKB <= 8 ? 4 : 8;
+}
+
+// One storage type: pick the instantiation for the plan's k-block bucket.
+template <typename T, int TILE, int MODE>
+hipError_t eval_dispatch(const MfmaPlan &pl, const MfmaArgs &x, hipStream_t st) {
+    if constexpr (TILE == 16) {
+        switch (pl.nkb) {
+        case 20: return eval_launch<T, TILE, 20, 4, 1, waves_for<20>(), MODE>(x, st);
+        case 24: return eval_launch<T, TILE, 24, 4, 1, waves_for<24>(), MODE>(x, st);
+        case 28: return eval_launch<T, TILE, 28, 4, 1, waves_for<28>(), MODE>(x, st);
+        case 32: return eval_launch<T, TILE, 32, 4, 1, waves_for<32>(), MODE>(x, st);
+        }
+    } else {
+        constexpr int KL = Mfma<T, TILE>::KS_PER_KB;
+        if (pl.nkb == 1) {
+            if constexpr (KL == 4) {
+                switch (pl.nks_last) {
+                case 1: return eval_launch<T, TILE, 1, 1, 2, waves_for<1>(), MODE>(x, st);
+                case 2: return eval_launch<T, TILE, 1, 2, 2, waves_for<1>(), MODE>(x, st);
+                case 3: return eval_launch<T, TILE, 1, 3, 2, waves_for<1>(), MODE>(x, st);
+                case 4: return eval_launch<T, TILE, 1, 4, 2, waves_for<1>(), MODE>(x, st);
+                }
+                return hipErrorInvalidValue;
+            } else {
+                return eval_launch<T, TILE, 1, KL, 2, waves_for<1>(), MODE>(x, st);
+            }
+        }
+        switch (pl.nkb) {
+        case 2: return eval_launch<T, TILE, 2, KL, 2, waves_for<2>(), MODE>(x, st);
+        case 3: return eval_launch<T, TILE, 3, KL, 2, waves_for<3>(), MODE>(x, st);
+        case 4: return eval_launch<T, TILE, 4, KL, 2, waves_for<4>(), MODE>(x, st);
+        case 5: return eval_launch<T, TILE, 5, KL, 2, waves_for<5>(), MODE>(x, st);
+        case 6: return eval_launch<T, TILE, 6, KL, 2, waves_for<6>(), MODE>(x, st);
+        case 7: return eval_launch<T, TILE, 7, KL, 2, waves_for<7>(), MODE>(x, st);
+        case 8: return eval_launch<T, TILE, 8, KL, 2, waves_for<8>(), MODE>(x, st);
+        case 10: return eval_launch<T, TILE, 10, KL, 2, waves_for<10>(), MODE>(x, st);
+        case 12: return eval_launch<T, TILE, 12, KL, 2, waves_for<12>(), MODE>(x, st);
+        case 13: return eval_launch<T, TILE, 13, KL, 2, waves_for<13>(), MODE>(x, st);
+        case 14: return eval_launch<T, TILE, 14, KL, 2, waves_for<14>(), MODE>(x, st);
+        case 16: return eval_launch<T, TILE, 16, KL, 2, waves_for<16>(), MODE>(x, st);
+        case 20: return eval_launch<T, TILE, 20, KL, 1, waves_for<20>(), MODE>(x, st);
+        case 24: return eval_launch<T, TILE, 24, KL, 1, waves_for<24>(), MODE>(x, st);
+        case 28: return eval_launch<T, TILE, 28, KL, 1, waves_for<28>(), MODE>(x, st);
+        case 32: return eval_launch<T, TILE, 32, KL, 1, waves_for<32>(), MODE>(x, st);
+        }
+    }
+    return hipErrorInvalidValue;
+}
+
+}  // namespace exemcl
