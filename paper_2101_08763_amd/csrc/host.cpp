@@ -84,7 +84,7 @@ bool layout_eval(int64_t n, int64_t d, int64_t l, int64_t k, int precision, int 
         L->off_partials = 0;
         L->off_tiles = align_up(L->G * L->lpad * 4, 256);
         L->off_aux = align_up(L->off_tiles + L->ngroups * k * tile_bytes(L->mp), 256);
-        L->bytes = L->off_aux;
+        L->bytes = align_up(L->off_aux + reduce_scratch_bytes(L->G, l), 256);
         return true;
     }
     if (path == EXEMCL_PATH_VALU) {
@@ -93,7 +93,7 @@ bool layout_eval(int64_t n, int64_t d, int64_t l, int64_t k, int precision, int 
         L->G = (n + L->vp.rows - 1) / L->vp.rows;
         L->off_partials = 0;
         L->off_aux = align_up(L->G * L->lpad * 4, 256);
-        L->bytes = L->off_aux;
+        L->bytes = align_up(L->off_aux + reduce_scratch_bytes(L->G, l), 256);
         return true;
     }
     L->bytes = 0;
@@ -231,7 +231,8 @@ int run_eval(const void *V, int64_t n, int64_t d, const int32_t *sets, int64_t l
         e = launch_valu(precision, L.vp, V, n, (int)d, sets, l, k, partials, L.lpad, st);
         pr.end();
     }
-    if (e == hipSuccess) e = launch_reduce(partials, L.G, L.lpad, l, n, sets, k, common, kcommon, out, st);
+    if (e == hipSuccess)
+        e = launch_reduce(partials, L.G, L.lpad, l, n, sets, k, common, kcommon, (double *)(base + L.off_aux), out, st);
     return status_of(e);
 }
 

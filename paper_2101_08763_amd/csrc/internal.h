@@ -84,9 +84,11 @@ hipError_t launch_valu(int prec, const ValuPlan &pl, const void *V, int64_t n, i
 
 // out[j] = (2/n) * sum_g partials[g * lpad + j] (fp64, fixed order), or NaN
 // when an index of set j (or of the common list) is outside [0, n).
+// `scratch` holds reduce_scratch_bytes(G, l) bytes.
+int64_t reduce_scratch_bytes(int64_t G, int64_t l);
 hipError_t launch_reduce(const float *partials, int64_t G, int64_t lpad, int64_t l, int64_t n,
                          const int32_t *sets, int64_t kset, const int32_t *common, int64_t kcommon,
-                         float *out, hipStream_t st);
+                         double *scratch, float *out, hipStream_t st);
 
 hipError_t launch_sqnorm(int prec, const void *V, int64_t n, int d, float *q, hipStream_t st);
 

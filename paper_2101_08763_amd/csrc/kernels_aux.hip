@@ -156,30 +156,40 @@ hipError_t launch_valu(int prec, const ValuPlan &pl, const void *V, int64_t n, i
 }
 
 // ---------------------------------------------------------------------------
-// Second pass: out[j] = (2/n) * sum_g partials[g][j].  Four fp64 running sums
-// over g = 0 mod 4, 1 mod 4, ... combined in a fixed tree, so the result does
-// not depend on how the partials were scheduled.  The index check turns a set
-// with an index outside [0, n) into NaN.
+// Second pass: out[j] = (2/n) * sum_g partials[g][j].
+//
+// Stage 1: the G partial rows are cut into chunks of rchunk(G) consecutive
+// rows; thread (j, c) adds chunk c of column j in fp64, in row order.  Stage 2 adds
+// the chunk sums of column j in chunk order.  The chunking depends on G only,
+// so the summation order of a set does not depend on the batch.  The index
+// check turns a set with an index outside [0, n) into NaN.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void reduce_partials_kernel(const float *__restrict__ partials, int64_t G,
-                                                              int64_t lpad, int64_t l, int64_t n,
-                                                              const int32_t *__restrict__ sets, int64_t kset,
-                                                              const int32_t *__restrict__ common, int64_t kcommon,
-                                                              float *__restrict__ out) {
+static int64_t rchunk(int64_t G) {
+    const int64_t c = (G + 65534) / 65535;  // keeps the chunk count within grid.y
+    return c > 32 ? c : 32;
+}
+
+__global__ __launch_bounds__(256) void reduce_chunks_kernel(const float *__restrict__ partials, int64_t G,
+                                                            int64_t lpad, int64_t l, int64_t rows_per_chunk,
+                                                            double *__restrict__ chunks) {
+    const int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    const int64_t c = blockIdx.y;
+    if (j >= l) return;
+    const int64_t g0 = c * rows_per_chunk;
+    const int64_t g1 = min(G, g0 + rows_per_chunk);
+    double s = 0.0;
+    for (int64_t g = g0; g < g1; ++g) s += (double)partials[g * lpad + j];
+    chunks[c * l + j] = s;
+}
+
+__global__ __launch_bounds__(256) void reduce_final_kernel(const double *__restrict__ chunks, int64_t nchunks,
+                                                           int64_t l, int64_t n, const int32_t *__restrict__ sets,
+                                                           int64_t kset, const int32_t *__restrict__ common,
+                                                           int64_t kcommon, float *__restrict__ out) {
     const int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x;
     if (j >= l) return;
-    double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
-    int64_t g = 0;
-    for (; g + 3 < G; g += 4) {
-        s0 += (double)partials[g * lpad + j];
-        s1 += (double)partials[(g + 1) * lpad + j];
-        s2 += (double)partials[(g + 2) * lpad + j];
-        s3 += (double)partials[(g + 3) * lpad + j];
-    }
-    if (g < G) s0 += (double)partials[g * lpad + j];
-    if (g + 1 < G) s1 += (double)partials[(g + 1) * lpad + j];
-    if (g + 2 < G) s2 += (double)partials[(g + 2) * lpad + j];
-    const double s = (s0 + s1) + (s2 + s3);
+    double s = 0.0;
+    for (int64_t c = 0; c < nchunks; ++c) s += chunks[c * l + j];
     bool bad = false;
     for (int64_t p = 0; p < kset; ++p) {
         const int64_t idx = sets[j * kset + p];
@@ -192,12 +202,24 @@ __global__ __launch_bounds__(256) void reduce_partials_kernel(const float *__res
     out[j] = bad ? __builtin_nanf("") : (float)(2.0 * s / (double)n);
 }
 
+int64_t reduce_scratch_bytes(int64_t G, int64_t l) {
+    return ((G + rchunk(G) - 1) / rchunk(G)) * l * (int64_t)sizeof(double);
+}
+
 hipError_t launch_reduce(const float *partials, int64_t G, int64_t lpad, int64_t l, int64_t n,
-                         const int32_t *sets, int64_t kset, const int32_t *common, int64_t kcommon, float *out,
-                         hipStream_t st) {
+                         const int32_t *sets, int64_t kset, const int32_t *common, int64_t kcommon, double *scratch,
+                         float *out, hipStream_t st) {
     const int64_t blocks = (l + 255) / 256;
-    hipLaunchKernelGGL(reduce_partials_kernel, dim3((unsigned)blocks), dim3(256), 0, st, partials, G, lpad, l, n,
-                       sets, kset, common, kcommon, out);
+    const int64_t rc = rchunk(G);
+    const int64_t nchunks = (G + rc - 1) / rc;
+    if (nchunks > 0) {
+        hipLaunchKernelGGL(reduce_chunks_kernel, dim3((unsigned)blocks, (unsigned)nchunks), dim3(256), 0, st,
+                           partials, G, lpad, l, rc, scratch);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    hipLaunchKernelGGL(reduce_final_kernel, dim3((unsigned)blocks), dim3(256), 0, st, scratch, nchunks, l, n, sets,
+                       kset, common, kcommon, out);
     return hipGetLastError();
 }
 
