@@ -32,11 +32,12 @@ _LIB = None
 
 
 def load(path: str | None = None) -> ctypes.CDLL:
-    """Open libexemcl.so (once).  Raises if it has not been built."""
+    """Open libexemcl.so (once; EXEMCL_LIB overrides the path).  Raises if it
+    has not been built."""
     global _LIB
     if _LIB is not None and path is None:
         return _LIB
-    p = path or LIB_PATH
+    p = path or os.environ.get("EXEMCL_LIB") or LIB_PATH
     if not os.path.exists(p):
         raise ImportError(f"{p} is missing: build it with `python -m paper_2101_08763_amd.build` "
                           "(or __graft_entry__.build()); there is no fallback implementation")

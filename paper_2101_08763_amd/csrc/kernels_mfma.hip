@@ -44,7 +44,7 @@ bool mfma_plan(int prec, int64_t d, MfmaPlan *p) {
         q.rt = q.nkb <= 16 ? 2 : 1;
     }
     if (q.nkb < 1) return false;
-    q.waves = q.nkb <= 8 ? 4 : 8;  // same rule as waves_for<NKB>() in the kernels
+    q.waves = q.nkb <= EXEMCL_BIG_NKB ? EXEMCL_SMALL_WAVES : EXEMCL_BIG_WAVES;  // as waves_for<NKB>()
     q.rows = q.waves * q.rt * q.tile;
     *p = q;
     return true;

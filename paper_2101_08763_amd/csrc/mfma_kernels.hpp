@@ -86,19 +86,41 @@ __global__ __launch_bounds__(64) void pack_tiles_kernel(const T *__restrict__ V,
     }
 }
 
-// Bytes of one LDS stage buffer: at least 16 KiB and one whole tile, a
-// multiple of one 16-byte load per thread.
+// Stage geometry, fixed at compile time per k-block bucket.  Workgroups of
+// EXEMCL_SMALL_WAVES wavefronts serve tiles of at most EXEMCL_BIG_NKB
+// k-blocks, EXEMCL_BIG_WAVES above.  A stage buffer holds at least
+// EXEMCL_STAGE_MIN bytes and one whole tile, rounded to one 16-byte load per
+// thread; the ring has EXEMCL_RING_SMALL / EXEMCL_RING_BIG buffers.
+#ifndef EXEMCL_SMALL_WAVES
+#define EXEMCL_SMALL_WAVES 4
+#endif
+#ifndef EXEMCL_BIG_WAVES
+#define EXEMCL_BIG_WAVES 8
+#endif
+#ifndef EXEMCL_BIG_NKB
+#define EXEMCL_BIG_NKB 8
+#endif
+#ifndef EXEMCL_STAGE_MIN
+#define EXEMCL_STAGE_MIN 16384
+#endif
+#ifndef EXEMCL_RING_SMALL
+#define EXEMCL_RING_SMALL 4
+#endif
+#ifndef EXEMCL_RING_BIG
+#define EXEMCL_RING_BIG 3
+#endif
+
 template <int NKB, int WAVES>
 constexpr int stage_bytes() {
     constexpr int per_round = WAVES * 64 * 16;
     constexpr int tb = tile_bytes_of<NKB>();
-    constexpr int need = tb > 16384 ? tb : 16384;
+    constexpr int need = tb > EXEMCL_STAGE_MIN ? tb : EXEMCL_STAGE_MIN;
     return (need + per_round - 1) / per_round * per_round;
 }
 
 template <int NKB>
 constexpr int ring_depth() {
-    return 3;
+    return NKB > 16 ? EXEMCL_RING_BIG : EXEMCL_RING_SMALL;
 }
 
 template <int N>
@@ -353,7 +375,7 @@ hipError_t eval_launch(const MfmaArgs &x, hipStream_t st) {
 // Wavefronts per workgroup for a k-block bucket (the plan uses the same rule).
 template <int NKB>
 constexpr int waves_for() {
-    return NKB <= 8 ? 4 : 8;
+    return NKB <= EXEMCL_BIG_NKB ? EXEMCL_SMALL_WAVES : EXEMCL_BIG_WAVES;
 }
 
 // One storage type: pick the instantiation for the plan's k-block bucket.
