@@ -88,9 +88,11 @@ __global__ __launch_bounds__(64) void pack_tiles_kernel(const T *__restrict__ V,
 
 // Stage geometry, fixed at compile time per k-block bucket.  Workgroups of
 // EXEMCL_SMALL_WAVES wavefronts serve tiles of at most EXEMCL_BIG_NKB
-// k-blocks, EXEMCL_BIG_WAVES above.  A stage buffer holds at least
-// EXEMCL_STAGE_MIN bytes and one whole tile, rounded to one 16-byte load per
-// thread; the ring has EXEMCL_RING_SMALL / EXEMCL_RING_BIG buffers.
+// k-blocks, EXEMCL_BIG_WAVES above.  Small tiles are batched into stages of
+// at least EXEMCL_STAGE_MIN bytes; large tiles go EXEMCL_TPS_BIG per stage.
+// A stage is rounded up to one 16-byte load per thread, at most two stages
+// share the 160 KiB of LDS, and the ring has up to EXEMCL_RING_SMALL /
+// EXEMCL_RING_BIG buffers.  Fewer, larger stages mean fewer barriers.
 #ifndef EXEMCL_SMALL_WAVES
 #define EXEMCL_SMALL_WAVES 4
 #endif
@@ -103,6 +105,9 @@ __global__ __launch_bounds__(64) void pack_tiles_kernel(const T *__restrict__ V,
 #ifndef EXEMCL_STAGE_MIN
 #define EXEMCL_STAGE_MIN 16384
 #endif
+#ifndef EXEMCL_TPS_BIG
+#define EXEMCL_TPS_BIG 4
+#endif
 #ifndef EXEMCL_RING_SMALL
 #define EXEMCL_RING_SMALL 4
 #endif
@@ -110,17 +115,31 @@ __global__ __launch_bounds__(64) void pack_tiles_kernel(const T *__restrict__ V,
 #define EXEMCL_RING_BIG 3
 #endif
 
+constexpr int kLdsBytes = 160 * 1024;
+
 template <int NKB, int WAVES>
-constexpr int stage_bytes() {
-    constexpr int per_round = WAVES * 64 * 16;
-    constexpr int tb = tile_bytes_of<NKB>();
-    constexpr int need = tb > EXEMCL_STAGE_MIN ? tb : EXEMCL_STAGE_MIN;
-    return (need + per_round - 1) / per_round * per_round;
+constexpr int round_stage(int bytes) {
+    return (bytes + WAVES * 1024 - 1) / (WAVES * 1024) * (WAVES * 1024);
 }
 
-template <int NKB>
+template <int NKB, int WAVES>
+constexpr int tiles_per_stage() {
+    constexpr int tb = tile_bytes_of<NKB>();
+    int tps = NKB <= EXEMCL_BIG_NKB ? (EXEMCL_STAGE_MIN / tb > 1 ? EXEMCL_STAGE_MIN / tb : 1) : EXEMCL_TPS_BIG;
+    while (tps > 1 && 2 * round_stage<NKB, WAVES>(tps * tb) > kLdsBytes) --tps;
+    return tps;
+}
+
+template <int NKB, int WAVES>
+constexpr int stage_bytes() {
+    return round_stage<NKB, WAVES>(tiles_per_stage<NKB, WAVES>() * tile_bytes_of<NKB>());
+}
+
+template <int NKB, int WAVES>
 constexpr int ring_depth() {
-    return NKB > 16 ? EXEMCL_RING_BIG : EXEMCL_RING_SMALL;
+    constexpr int want = NKB <= EXEMCL_BIG_NKB ? EXEMCL_RING_SMALL : EXEMCL_RING_BIG;
+    constexpr int fit = kLdsBytes / stage_bytes<NKB, WAVES>();
+    return want < fit ? want : fit;
 }
 
 template <int N>
@@ -166,11 +185,12 @@ __global__ __launch_bounds__(WAVES * 64) void eval_mfma_kernel(const T *__restri
     constexpr int NT = WAVES * 64;
     constexpr int TB = tile_bytes_of<NKB>();
     constexpr int SB = stage_bytes<NKB, WAVES>();
-    constexpr int TPS = SB / TB;
+    constexpr int TPS = tiles_per_stage<NKB, WAVES>();
     constexpr int CNT = SB / (NT * 16);
-    constexpr int NBUF = ring_depth<NKB>();
+    constexpr int NBUF = ring_depth<NKB, WAVES>();
     constexpr int PF = NKB < 3 ? NKB : 3;  // B fragments in flight ahead of use
-    static_assert(TPS >= 1 && NBUF >= 2, "stage geometry");
+    static_assert(TPS >= 1 && TPS * TB <= SB && NBUF >= 2 && NBUF * SB <= kLdsBytes, "stage geometry");
+    static_assert(CNT * (NBUF - 2) < 64, "vmcnt range");
     static_assert(NKS_LAST >= 1 && NKS_LAST <= M::KS_PER_KB, "k-steps of the last block");
 
     extern __shared__ __align__(16) unsigned char smem[];
@@ -347,7 +367,7 @@ hipError_t pack_launch(const MfmaPlan &pl, const void *V, int64_t n, int d, cons
 template <typename T, int TILE, int NKB, int NKS_LAST, int RT, int WAVES, int MODE, bool HAS_M0>
 hipError_t eval_launch_t(const MfmaArgs &x, hipStream_t st) {
     constexpr int SB = stage_bytes<NKB, WAVES>();
-    constexpr int NBUF = ring_depth<NKB>();
+    constexpr int NBUF = ring_depth<NKB, WAVES>();
     auto kern = eval_mfma_kernel<T, TILE, NKB, NKS_LAST, RT, WAVES, MODE, HAS_M0>;
     const size_t lds = (size_t)NBUF * SB;
     if (lds > 64 * 1024) {
