@@ -13,9 +13,13 @@ Default workload: 50 000 points of a 10-Gaussian mixture in d = 32 (fp32),
 from __future__ import annotations
 
 import argparse
+import csv
+import glob
+import hashlib
 import json
 import os
 import platform
+import statistics
 import sys
 import time
 
@@ -27,6 +31,8 @@ sys.path.insert(0, ROOT)
 from paper_2101_08763_amd import api, synth  # noqa: E402
 
 METRIC = "set evaluations/s and distance terms/s (n·k·l) + % of MFMA/HBM peak"
+COPY_PROBE_BYTES = 1 << 30   # plain device copy used to calibrate the HBM byte counters
+PROFILES = os.path.join(ROOT, "profiles")
 PEAK_TFLOPS = {"fp32": 157.3, "fp16": 2516.6, "bf16": 2516.6}  # dense MFMA, MI355X
 DTYPE_NAME = {"fp32": "f32", "fp16": "f16", "bf16": "bf16"}
 
@@ -71,17 +77,102 @@ def cpu_baseline(p: synth.Problem, X64: np.ndarray, budget_s: float):
         per = (time.perf_counter() - t0) / len(probe)
         m = int(max(1, min(len(p.sets), budget_s / max(per, 1e-9))))
         idx = np.unique((np.arange(m) * (len(p.sets) - 1)) // max(m - 1, 1))
+        # Whole batches are repeated until the budget is used, for a stable rate.
+        passes = 0
         t0 = time.perf_counter()
-        o.eval(X64, p.sets[idx], threads)
-        dt = time.perf_counter() - t0
+        while True:
+            o.eval(X64, p.sets[idx], threads)
+            passes += 1
+            dt = time.perf_counter() - t0
+            if dt >= 0.5 * budget_s or len(idx) < w.l:
+                break
         kk = w.k
-    m = len(idx)
-    sample = "all sets" if m == w.l else f"strided sample of {m} of {w.l} sets"
+    m = len(idx) * (passes if w.mode == "eval" else 1)
+    sample = ("all sets" if len(idx) == w.l else f"strided sample of {len(idx)} of {w.l} sets")
+    if w.mode == "eval" and passes > 1:
+        sample += f", {passes} passes"
     return {
         "value": m / dt, "unit": "set evaluations/s", "cores": threads, "kind": "oracle",
         "sample": f"{sample}, fp64 direct evaluation, OpenMP over sets, {threads} threads on {cpu_model()}",
         "seconds": dt, "distance_terms_per_s": w.n * kk * m / dt,
     }
+
+
+def kernel_source_hash() -> str:
+    """Hash of everything that defines the compiled kernels (sources, build flags)."""
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2101_08763_amd", "csrc")
+    for f in sorted(os.listdir(csrc)) + ["../build.py"]:
+        with open(os.path.join(csrc, f), "rb") as fh:
+            h.update(f.encode())
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def traffic_file(kernel: str, workload: str) -> str:
+    return os.path.join(PROFILES, f"{kernel}__{workload}.traffic.json")
+
+
+def load_traffic(kernel: str, workload: str):
+    """HBM bytes per launch from the committed counter runs, or None when the
+    kernel sources changed since they were taken (or none were taken)."""
+    path = traffic_file(kernel, workload)
+    if not os.path.exists(path):
+        return None
+    t = json.load(open(path))
+    if t.get("source_sha256") != kernel_source_hash():
+        return None
+    return t["hbm_bytes_per_launch"]
+
+
+def _pmc_values(run_dir: str, counter: str, name_re: str):
+    import re
+    vals = []
+    for f in glob.glob(os.path.join(run_dir, "**", "*counter_collection.csv"), recursive=True):
+        for r in csv.DictReader(open(f)):
+            if r["Counter_Name"] == counter and re.search(name_re, r["Kernel_Name"]):
+                vals.append(float(r["Counter_Value"]))
+    return vals
+
+
+def traffic_summary(d: str, kernel: str, workload: str) -> dict:
+    """Turn four rocprofv3 --pmc runs under d/ (fetch, write: the workload;
+    copy_fetch, copy_write: --copy-probe) into the committed traffic file."""
+    kf = _pmc_values(os.path.join(d, "fetch"), "FETCH_SIZE", kernel)
+    kw = _pmc_values(os.path.join(d, "write"), "WRITE_SIZE", kernel)
+    cf = _pmc_values(os.path.join(d, "copy_fetch"), "FETCH_SIZE", "copyBuffer")
+    cw = _pmc_values(os.path.join(d, "copy_write"), "WRITE_SIZE", "copyBuffer")
+    if not (kf and kw and cf and cw):
+        raise SystemExit(f"missing counter data under {d}")
+    fetch_kib, write_kib = statistics.median(kf), statistics.median(kw)
+    cfetch_kib, cwrite_kib = statistics.median(cf), statistics.median(cw)
+    ff = COPY_PROBE_BYTES / (cfetch_kib * 1024)
+    wf = COPY_PROBE_BYTES / (cwrite_kib * 1024)
+    out = {
+        "kernel": kernel, "workload": workload, "source_sha256": kernel_source_hash(),
+        "fetch_kib_per_dispatch": fetch_kib, "write_kib_per_dispatch": write_kib,
+        "copy_probe_bytes": COPY_PROBE_BYTES, "copy_fetch_kib": cfetch_kib, "copy_write_kib": cwrite_kib,
+        "fetch_scale": ff, "write_scale": wf,
+        "hbm_bytes_per_launch": fetch_kib * 1024 * ff + write_kib * 1024 * wf,
+        "dispatches": {"fetch": len(kf), "write": len(kw), "copy_fetch": len(cf), "copy_write": len(cw)},
+    }
+    os.makedirs(PROFILES, exist_ok=True)
+    with open(traffic_file(kernel, workload), "w") as fh:
+        json.dump(out, fh, indent=1)
+    return out
+
+
+def copy_probe(steps: int):
+    """A plain device-to-device copy of COPY_PROBE_BYTES (calibration target
+    for FETCH_SIZE / WRITE_SIZE)."""
+    import torch
+    n = COPY_PROBE_BYTES // 4
+    src = torch.ones(n, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(steps):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_probe_bytes": COPY_PROBE_BYTES, "launches": steps}))
 
 
 def main():
@@ -92,7 +183,15 @@ def main():
     ap.add_argument("--workload", default="mix50k", choices=sorted(synth.WORKLOADS))
     ap.add_argument("--cpu-budget", type=float, default=10.0, help="seconds of oracle time for the CPU baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe", action="store_true", help="run a plain 1 GiB device copy (counter calibration)")
+    ap.add_argument("--traffic-summary", metavar="DIR",
+                    help="summarise rocprofv3 FETCH_SIZE/WRITE_SIZE runs under DIR into profiles/")
+    ap.add_argument("--kernel", default="eval_mfma_kernel", help="kernel name for --traffic-summary")
     args = ap.parse_args()
+
+    if args.traffic_summary:
+        print(json.dumps(traffic_summary(args.traffic_summary, args.kernel, args.workload)))
+        return
 
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); the library has no multi-GPU "
@@ -103,9 +202,12 @@ def main():
 
     if not torch.cuda.is_available():
         sys.exit("bench.py needs a GPU")
-    api.load()
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.copy_probe:
+        copy_probe(max(args.steps, 1))
+        return
+    api.load()
 
     w = synth.WORKLOADS[args.workload]
     log(f"generating {w.name}: {w.note}")
@@ -181,7 +283,8 @@ def main():
         },
         "roofline": {
             "bound": "mfma", "achieved": achieved, "peak": peak, "unit": "TFLOP/s", "frac": achieved / peak,
-            "traffic": None, "kernel": "eval_mfma_kernel" if path == "mfma" else "eval_valu_kernel",
+            "traffic": load_traffic("eval_mfma_kernel" if path == "mfma" else "eval_valu_kernel", w.name),
+            "kernel": "eval_mfma_kernel" if path == "mfma" else "eval_valu_kernel",
             "kernel_avg_us": kern_avg_ms * 1e3, "flops_per_launch": flops_per_launch,
         },
     }
