@@ -103,13 +103,13 @@ __global__ __launch_bounds__(64) void pack_tiles_kernel(const T *__restrict__ V,
 #define EXEMCL_BIG_NKB 8
 #endif
 #ifndef EXEMCL_STAGE_MIN
-#define EXEMCL_STAGE_MIN 16384
+#define EXEMCL_STAGE_MIN 24576
 #endif
 #ifndef EXEMCL_TPS_BIG
 #define EXEMCL_TPS_BIG 4
 #endif
 #ifndef EXEMCL_RING_SMALL
-#define EXEMCL_RING_SMALL 4
+#define EXEMCL_RING_SMALL 2
 #endif
 #ifndef EXEMCL_RING_BIG
 #define EXEMCL_RING_BIG 3
