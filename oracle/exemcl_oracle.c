@@ -27,8 +27,11 @@
  *
  * Readings where the paper is silent (each listed in the design notes):
  *   - sets are given as int32 row indices into V (S is a subset of V);
- *   - a set holding an index outside [0, n) has no defined value: its result
- *     is a quiet NaN and the other sets are unaffected;
+ *   - sets of different sizes share one k by padding with the index -1, an
+ *     empty slot that is not a member (the blank fields of the evaluation-set
+ *     matrix, Section IV-B, Memory Layout);
+ *   - a set holding any other index outside [0, n) has no defined value: its
+ *     result is a quiet NaN and the other sets are unaffected;
  *   - duplicate indices are allowed (the minimum is idempotent);
  *   - n = 0 is rejected (L would be 0/0).
  *
@@ -49,6 +52,9 @@
 #endif
 
 enum { ORACLE_OK = 0, ORACLE_EINVAL = 1, ORACLE_ENOMEM = 2 };
+
+/* Padding index of a set shorter than the batch's k. */
+#define EMPTY_SLOT (-1)
 
 /* Row i of the row-major n x d matrix V. */
 static const double *row(const double *V, int64_t d, int64_t i) { return V + i * d; }
@@ -76,13 +82,14 @@ static double dissim(const double *x, const double *y, int64_t d) {
  * L(X) of Eq. (3) for X = {members of `idx`} u {e0}, computed as in
  * Algorithm 2's function L: per point a running minimum started at the
  * largest double, a stored minimum per point, then the sum and the division
- * by |V|.  e0 is compared first, then the indexed members in slot order.
- * Returns NaN when an index is out of range.
+ * by |V|.  e0 is compared first, then the indexed members in slot order;
+ * empty slots (-1) are skipped.  Returns NaN when another index is out of
+ * range.
  */
 static double loss(const double *V, int64_t n, int64_t d, const double *e0, const int32_t *idx,
                    int64_t k, double *scratch) {
     for (int64_t p = 0; p < k; ++p)
-        if (idx[p] < 0 || (int64_t)idx[p] >= n) return NAN;
+        if (idx[p] != EMPTY_SLOT && (idx[p] < 0 || (int64_t)idx[p] >= n)) return NAN;
 
     for (int64_t i = 0; i < n; ++i) {
         const double *v = row(V, d, i);
@@ -105,6 +112,7 @@ static double loss(const double *V, int64_t n, int64_t d, const double *e0, cons
 #else
         for (int64_t p = 0; p < k; ++p) {
 #endif
+            if (idx[p] == EMPTY_SLOT) continue; /* a blank field: no member */
             double ds = dissim(v, row(V, d, idx[p]), d);
 #if ORACLE_MUTANT == 7
             t = fmax(t, ds);

@@ -178,14 +178,33 @@ def pin_threads_and_gain(o):
 
 
 def pin_invalid_index(o):
-    """An index outside [0, n) poisons only its own set."""
+    """An index outside [0, n) other than the empty slot -1 poisons only its
+    own set."""
     V = _rng_points(13, 20, 3)
-    sets = np.array([[1, 2], [3, 20], [-1, 0], [4, 5]], np.int32)
+    sets = np.array([[1, 2], [3, 20], [-2, 0], [4, 5]], np.int32)
     got = o.eval(V, sets, 1)
     assert np.isnan(got[1]) and np.isnan(got[2]), "out-of-range index"
     _close(got[[0, 3]], o.eval(V, sets[[0, 3]], 1), what="other sets")
 
 
+def pin_empty_slots(o):
+    """Sets of different sizes padded with -1 (blank fields) score exactly as
+    the unpadded sets; an all-blank set scores f(empty) = 0."""
+    rng = np.random.default_rng(14)
+    V = rng.standard_normal((60, 2))
+    sizes = [4, 3, 5, 0, 1]
+    k = max(sizes)
+    padded = np.full((len(sizes), k), -1, np.int32)
+    want = []
+    for j, sz in enumerate(sizes):
+        members = rng.choice(60, sz, replace=False).astype(np.int32)
+        padded[j, :sz] = members
+        rng.shuffle(padded[j])
+        want.append(o.eval(V, members[None, :], 1)[0] if sz else 0.0)
+    got = o.eval(V, padded, 1)
+    assert np.array_equal(got, np.asarray(want)), f"blank fields: {got} vs {want}"
+
+
 PINS = [pin_worked_examples, pin_empty_and_full, pin_monotone_submodular_bruteforce,
         pin_kdtree_nearest_neighbour, pin_closed_forms, pin_scaling_and_order,
-        pin_threads_and_gain, pin_invalid_index]
+        pin_threads_and_gain, pin_invalid_index, pin_empty_slots]
