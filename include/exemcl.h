@@ -25,9 +25,12 @@
  *   - V is dense row-major n x d (row stride d elements, no padding), with
  *     element type fp32, fp16 or bf16 as selected by `precision`.  Results are
  *     fp32.  Arithmetic is fp32 (fp16/bf16 products are exact in fp32).
- *   - Sets are int32 row indices into V.  Duplicate indices are allowed.  An
- *     index outside [0, n) makes that set's result a quiet NaN and leaves the
- *     other results untouched (detected on the device, no sync).
+ *   - Sets are int32 row indices into V.  Duplicate indices are allowed.
+ *     EXEMCL_EMPTY_SLOT (-1) marks an empty slot, so sets of different sizes
+ *     share one k (the blank fields of the paper's evaluation-set matrix,
+ *     Section IV-B, Memory Layout).  Any other index outside [0, n) makes
+ *     that set's result a quiet NaN and leaves the other results untouched
+ *     (detected on the device, no sync).
  *   - The return value is a status, decided on the host before any kernel
  *     runs (EINVAL, ENOMEM) or right after the launches (EDEVICE).
  *   - Every result is bitwise reproducible and independent of the batch it
@@ -48,6 +51,9 @@ extern "C" {
 #else
 #define EXEMCL_API
 #endif
+
+/* Padding index of a set shorter than the batch's k. */
+#define EXEMCL_EMPTY_SLOT (-1)
 
 /* Storage type of V. */
 enum exemcl_precision { EXEMCL_FP32 = 0, EXEMCL_FP16 = 1, EXEMCL_BF16 = 2 };
@@ -71,7 +77,8 @@ enum exemcl_path {
  * exemplar_eval -- f(S_j) for a batch of l sets of k exemplars each.
  *
  * Computes out[j] = f(S_j) = L({e0}) - L(S_j u {e0}) (Eq. (3), Eq. (4)) for
- * S_j = { V[sets[j*k + p]] : p < k }, the multiset evaluation of Section IV-A.
+ * S_j = { V[sets[j*k + p]] : p < k, sets[j*k + p] != EXEMCL_EMPTY_SLOT }, the
+ * multiset evaluation of Section IV-A.
  * Internally the value is formed as (2/n) * sum_v max(0, max_{s in S_j}
  * (<v,s> - ||s||^2/2)), which equals the definition exactly in real
  * arithmetic and avoids subtracting two nearly equal losses.

@@ -9,6 +9,9 @@ namespace exemcl {
 
 enum Prec { P_FP32 = 0, P_FP16 = 1, P_BF16 = 2 };
 
+// Index of an empty slot: pads sets shorter than the batch's k.
+constexpr int32_t kEmptySlot = -1;
+
 // Geometry of one MFMA evaluation launch; a pure function of (d, precision),
 // never of n or l, so that the partial-sum layout seen by one set does not
 // depend on the batch it arrives in.

@@ -193,11 +193,11 @@ __global__ __launch_bounds__(256) void reduce_final_kernel(const double *__restr
     bool bad = false;
     for (int64_t p = 0; p < kset; ++p) {
         const int64_t idx = sets[j * kset + p];
-        bad |= idx < 0 || idx >= n;
+        bad |= idx != kEmptySlot && (idx < 0 || idx >= n);
     }
     for (int64_t p = 0; p < kcommon; ++p) {
         const int64_t idx = common[p];
-        bad |= idx < 0 || idx >= n;
+        bad |= idx != kEmptySlot && (idx < 0 || idx >= n);
     }
     out[j] = bad ? __builtin_nanf("") : (float)(2.0 * s / (double)n);
 }

@@ -193,7 +193,7 @@ def test_edge_cases(torch_gpu, orc):
     e = api.exemplar_eval(Vg, torch.zeros((0, 3), dtype=torch.int32, device="cuda"))
     assert e.numel() == 0
     # invalid indices poison their own set only
-    sets = np.array([[1, 2, 3], [4, 300, 5], [-1, 0, 1], [7, 8, 9]], np.int32)
+    sets = np.array([[1, 2, 3], [4, 300, 5], [-3, 0, 1], [7, 8, 9]], np.int32)
     got = gpu_eval(torch, Vg, sets)
     assert np.isnan(got[1]) and np.isnan(got[2]) and np.isfinite(got[[0, 3]]).all()
     check(got, orc.eval(X64, sets), le0, "fp32", "invalid")
@@ -294,3 +294,50 @@ def test_paths_agree(torch_gpu, orc, monkeypatch):
     monkeypatch.setenv("EXEMCL_PATH", "mfma")
     b = gpu_eval(torch, Vg, p.sets)
     check(a, b, orc.loss_e0(X64), "fp32", "valu vs mfma")
+
+
+# ---------------------------------------------------------------------------
+# Sets of different sizes in one batch: -1 pads the short ones (the blank
+# fields of the evaluation-set matrix).
+# ---------------------------------------------------------------------------
+def _padded_sets(rng, n, sizes):
+    k = max(sizes)
+    sets = np.full((len(sizes), k), -1, np.int32)
+    for j, sz in enumerate(sizes):
+        sets[j, :sz] = rng.choice(n, sz, replace=False)
+        rng.shuffle(sets[j])
+    return sets
+
+
+def test_variable_size_paper_figure(torch_gpu, orc):
+    """Three sets of sizes 4, 3 and 5 in d = 2, the shape of the paper's
+    evaluation-set matrix figure."""
+    rng = np.random.default_rng(425)
+    X = rng.standard_normal((500, 2)).astype(np.float32)
+    sets = _padded_sets(rng, 500, [4, 3, 5])
+    Vg, X64 = to_gpu(torch_gpu, X, "fp32")
+    want = orc.eval(X64, sets)
+    for j, sz in enumerate([4, 3, 5]):
+        members = sets[j][sets[j] >= 0]
+        assert len(members) == sz
+        assert abs(want[j] - orc.eval(X64, members[None])[0]) <= 1e-12 * abs(want[j])
+    check(gpu_eval(torch_gpu, Vg, sets), want, orc.loss_e0(X64), "fp32", "figure sizes")
+
+
+@pytest.mark.parametrize("path", ["mfma", "valu"])
+@pytest.mark.parametrize("prec,d", [("fp32", 3), ("fp32", 32), ("fp16", 128), ("bf16", 16)])
+def test_variable_size_batches(torch_gpu, orc, monkeypatch, path, prec, d):
+    if path == "valu" and d > 16:
+        pytest.skip("VALU path covers d <= 16")
+    monkeypatch.setenv("EXEMCL_PATH", path)
+    rng = np.random.default_rng(d)
+    p = synth.random_problem(3000, d, 1, 1, seed=d, clusters=3)
+    sizes = list(rng.integers(0, 12, size=75))
+    sizes[0] = 11
+    sets = _padded_sets(rng, 3000, sizes)
+    sets[5, 0] = -7  # a genuinely invalid index still gives NaN
+    Vg, X64 = to_gpu(torch_gpu, p.X, prec)
+    got = gpu_eval(torch_gpu, Vg, sets)
+    check(got, orc.eval(X64, sets, 8), orc.loss_e0(X64), prec, f"variable sizes {path} d={d}")
+    empty = [j for j, sz in enumerate(sizes) if sz == 0 and j != 5]
+    assert np.all(got[empty] == 0.0)
