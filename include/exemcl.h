@@ -94,10 +94,13 @@ enum exemcl_path {
  *   stream     hipStream_t or NULL
  *
  * Errors: EINVAL for a NULL array with a non-zero size, n < 1, n > INT32_MAX,
- * d < 1, d > 512, k < 0, l < 0 or an unknown precision; ENOMEM when the temporary
- * buffers (partial sums and staged exemplar tiles, O(l*k*d) bytes) cannot be
- * allocated -- the analogue of the paper's chunking failure (Section IV-B,
- * Chunking); EDEVICE when a launch fails.
+ * d < 1, d > 512, k < 0, l < 0 or an unknown precision; EDEVICE when a
+ * launch fails.  Temporary buffers (partial sums and staged exemplar tiles,
+ * O(l*k*d) bytes) come from the library's pool; when the whole batch does not
+ * fit (or exceeds EXEMCL_WORKSPACE_LIMIT bytes), the batch is processed in
+ * chunks of whole set groups, with bitwise the same results (Section IV-B,
+ * Chunking).  ENOMEM only when not even one group of 32 sets fits -- the
+ * paper's chunk size 0.
  */
 EXEMCL_API int exemplar_eval(const void *V, int64_t n, int64_t d, const int32_t *sets, int64_t l,
                              int64_t k, int precision, float *out, void *stream);

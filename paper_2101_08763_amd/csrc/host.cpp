@@ -201,23 +201,13 @@ struct ProfRange {
     }
 };
 
-// Queue one evaluation of `l` sets of `k` members (shared by eval and the
-// scoring half of gain).  `m0` (nullable) is the per-point initial max.
-int run_eval(const void *V, int64_t n, int64_t d, const int32_t *sets, int64_t l, int64_t k, int precision,
-             const float *m0, const int32_t *common, int64_t kcommon, float *out, hipStream_t st) {
-    if (l == 0) return EXEMCL_OK;
-    int path = k == 0 ? EXEMCL_PATH_NONE : choose_path(d, k, precision);
-    if (m0 && path == EXEMCL_PATH_VALU) path = EXEMCL_PATH_MFMA;
-    if (k > 0 && path == EXEMCL_PATH_NONE) return EXEMCL_EINVAL;
-    Layout L;
-    if (!layout_eval(n, d, l, k, precision, path, &L)) return EXEMCL_EINVAL;
-    Scratch ws;
-    int rc = alloc_scratch(&ws, L.bytes, st);
-    if (rc) return rc;
-    char *base = (char *)ws.ptr;
+// Queue the evaluation of sets [0, l) with a workspace laid out by L.
+hipError_t run_chunk(const Layout &L, char *base, const void *V, int64_t n, int64_t d, const int32_t *sets,
+                     int64_t l, int64_t k, int precision, const float *m0, const int32_t *common, int64_t kcommon,
+                     float *out, hipStream_t st) {
     float *partials = (float *)(base + L.off_partials);
     hipError_t e = hipSuccess;
-    if (path == EXEMCL_PATH_MFMA) {
+    if (L.path == EXEMCL_PATH_MFMA) {
         void *tiles = base + L.off_tiles;
         e = launch_pack(precision, L.mp, V, n, (int)d, sets, l, k, tiles, st);
         if (e == hipSuccess) {
@@ -226,14 +216,58 @@ int run_eval(const void *V, int64_t n, int64_t d, const int32_t *sets, int64_t l
                             L.lpad, nullptr, st);
             pr.end();
         }
-    } else if (path == EXEMCL_PATH_VALU) {
+    } else if (L.path == EXEMCL_PATH_VALU) {
         ProfRange pr(st);
         e = launch_valu(precision, L.vp, V, n, (int)d, sets, l, k, partials, L.lpad, st);
         pr.end();
     }
     if (e == hipSuccess)
-        e = launch_reduce(partials, L.G, L.lpad, l, n, sets, k, common, kcommon, (double *)(base + L.off_aux), out, st);
-    return status_of(e);
+        e = launch_reduce(partials, L.G, L.lpad, l, n, sets, k, common, kcommon, (double *)(base + L.off_aux), out,
+                          st);
+    return e;
+}
+
+// Queue one evaluation of `l` sets of `k` members (shared by eval and the
+// scoring half of gain).  `m0` (nullable) is the per-point initial max.
+//
+// Chunking (Section IV-B, Chunking): when the temporary memory for all l sets
+// is not available (EXEMCL_WORKSPACE_LIMIT, or the pool cannot grow), the
+// batch is split into chunks of whole set groups that fit, processed one
+// after another in one workspace.  A set's result does not depend on the
+// batch it is evaluated in, so chunked results are bitwise the same.  ENOMEM
+// only when not even one set group fits -- the paper's chunk size 0.
+int run_eval(const void *V, int64_t n, int64_t d, const int32_t *sets, int64_t l, int64_t k, int precision,
+             const float *m0, const int32_t *common, int64_t kcommon, float *out, hipStream_t st) {
+    if (l == 0) return EXEMCL_OK;
+    int path = k == 0 ? EXEMCL_PATH_NONE : choose_path(d, k, precision);
+    if (m0 && path == EXEMCL_PATH_VALU) path = EXEMCL_PATH_MFMA;
+    if (k > 0 && path == EXEMCL_PATH_NONE) return EXEMCL_EINVAL;
+    Layout L;
+    if (!layout_eval(n, d, l, k, precision, path, &L)) return EXEMCL_EINVAL;
+    const int64_t unit = path == EXEMCL_PATH_MFMA ? L.mp.tile : 1;
+    const int64_t limit = workspace_limit();
+    int64_t lc = l;
+    Scratch ws;
+    for (;;) {
+        if (!layout_eval(n, d, lc, k, precision, path, &L)) return EXEMCL_EINVAL;
+        if (L.bytes <= limit) {
+            const int rc = alloc_scratch(&ws, L.bytes, st);
+            if (rc == EXEMCL_OK) break;
+            if (rc != EXEMCL_ENOMEM) return rc;
+        }
+        if (lc <= unit) return EXEMCL_ENOMEM;
+        lc = ((lc + 1) / 2 + unit - 1) / unit * unit;
+    }
+    char *base = (char *)ws.ptr;
+    for (int64_t j0 = 0; j0 < l; j0 += lc) {
+        const int64_t lj = l - j0 < lc ? l - j0 : lc;
+        Layout Lj;
+        if (!layout_eval(n, d, lj, k, precision, path, &Lj)) return EXEMCL_EINVAL;
+        const hipError_t e = run_chunk(Lj, base, V, n, d, sets + j0 * k, lj, k, precision, m0, common, kcommon,
+                                       out + j0, st);
+        if (e != hipSuccess) return EXEMCL_EDEVICE;
+    }
+    return EXEMCL_OK;
 }
 
 }  // namespace

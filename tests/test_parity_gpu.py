@@ -341,3 +341,40 @@ def test_variable_size_batches(torch_gpu, orc, monkeypatch, path, prec, d):
     check(got, orc.eval(X64, sets, 8), orc.loss_e0(X64), prec, f"variable sizes {path} d={d}")
     empty = [j for j, sz in enumerate(sizes) if sz == 0 and j != 5]
     assert np.all(got[empty] == 0.0)
+
+
+# ---------------------------------------------------------------------------
+# Chunking: a workspace cap splits the batch into chunks of set groups.
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("prec,d", [("fp32", 32), ("fp16", 256), ("fp32", 5)])
+def test_chunked_batches_are_bitwise_equal(torch_gpu, orc, monkeypatch, prec, d):
+    torch = torch_gpu
+    p = synth.random_problem(9000, d, 300, 7, seed=50 + d, clusters=4)
+    Vg, X64 = to_gpu(torch, p.X, prec)
+    monkeypatch.delenv("EXEMCL_WORKSPACE_LIMIT", raising=False)
+    full = gpu_eval(torch, Vg, p.sets)
+    code = {"fp32": api.EXEMCL_FP32, "fp16": api.EXEMCL_FP16}[prec]
+    _, ws_all = api.exemplar_plan(9000, d, 300, 7, code)
+    _, ws_one = api.exemplar_plan(9000, d, 32, 7, code)
+    monkeypatch.setenv("EXEMCL_WORKSPACE_LIMIT", str(max(ws_one, ws_all // 3)))
+    chunked = gpu_eval(torch, Vg, p.sets)
+    assert np.array_equal(full, chunked)
+    check(chunked, orc.eval(X64, p.sets, 8), orc.loss_e0(X64), prec, "chunked")
+    monkeypatch.setenv("EXEMCL_WORKSPACE_LIMIT", str(ws_one - 1))
+    with pytest.raises(api.ExemclError) as ei:
+        gpu_eval(torch, Vg, p.sets)
+    assert ei.value.status == api.EXEMCL_ENOMEM
+
+
+def test_chunked_gain(torch_gpu, monkeypatch):
+    torch = torch_gpu
+    p = synth.random_problem(7000, 24, 1, 1, seed=60, clusters=3)
+    Vg, _ = to_gpu(torch, p.X, "fp32")
+    S = torch.tensor([5, 900, 4000], dtype=torch.int32, device="cuda")
+    C = torch.arange(0, 7000, 7, dtype=torch.int32, device="cuda")
+    monkeypatch.delenv("EXEMCL_WORKSPACE_LIMIT", raising=False)
+    full = api.exemplar_gain(Vg, S, C).cpu().numpy()
+    _, ws = api.exemplar_plan(7000, 24, C.numel(), 1)
+    monkeypatch.setenv("EXEMCL_WORKSPACE_LIMIT", str(ws // 4))
+    chunked = api.exemplar_gain(Vg, S, C).cpu().numpy()
+    assert np.array_equal(full, chunked)
