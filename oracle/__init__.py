@@ -60,6 +60,8 @@ class Oracle:
         lib.oracle_sqnorm.restype = ctypes.c_int
         lib.oracle_loss_e0.argtypes = [dp, i64, i64]
         lib.oracle_loss_e0.restype = ctypes.c_double
+        lib.oracle_greedy.argtypes = [dp, i64, i64, i64, ip, dp, ctypes.c_int]
+        lib.oracle_greedy.restype = ctypes.c_int
         lib.oracle_threads.argtypes = [ctypes.c_int]
         lib.oracle_threads.restype = ctypes.c_int
         self._lib = lib
@@ -109,6 +111,17 @@ class Oracle:
         if rc != OK:
             raise RuntimeError(f"oracle_gain failed with status {rc}")
         return out
+
+    def greedy(self, V, K: int, nthreads: int = 0):
+        """Algorithm 1: (indices added per round, f(S_i) after each round)."""
+        V = self._mat(V)
+        S = np.zeros(K, dtype=np.int32)
+        f = np.zeros(K, dtype=np.float64)
+        rc = self._lib.oracle_greedy(self._p(V, ctypes.c_double), V.shape[0], V.shape[1], int(K),
+                                     self._p(S, ctypes.c_int32), self._p(f, ctypes.c_double), int(nthreads))
+        if rc != OK:
+            raise RuntimeError(f"oracle_greedy failed with status {rc}")
+        return S, f
 
     def sqnorm(self, V) -> np.ndarray:
         V = self._mat(V)

@@ -255,3 +255,38 @@ int oracle_sqnorm(const double *V, int64_t n, int64_t d, double *q) {
 
 /* Number of OpenMP threads an nthreads request resolves to. */
 int oracle_threads(int nthreads) { return set_threads(nthreads); }
+
+/*
+ * The Greedy optimizer of Algorithm 1 on f: K rounds, each adding the point
+ * e in V \ S with the largest f(S u {e}) (equivalently the largest discrete
+ * derivative of Definition 1), evaluated directly by the definition.  Ties go
+ * to the lowest index (the paper leaves the tie-break open).  S_out[i] is the
+ * point added in round i, f_out[i] = f(S_i).
+ */
+int oracle_greedy(const double *V, int64_t n, int64_t d, int64_t K, int32_t *S_out, double *f_out,
+                  int nthreads) {
+    if (!V || n <= 0 || d <= 0 || K < 0 || K > n) return ORACLE_EINVAL;
+    if (K > 0 && (!S_out || !f_out)) return ORACLE_EINVAL;
+    int32_t *cands = (int32_t *)malloc((size_t)n * sizeof(int32_t));
+    double *score = (double *)malloc((size_t)n * sizeof(double));
+    char *taken = (char *)calloc((size_t)n, 1);
+    int rc = ORACLE_OK;
+    if (!cands || !score || !taken) rc = ORACLE_ENOMEM;
+    for (int64_t i = 0; rc == ORACLE_OK && i < K; ++i) {
+        int64_t m = 0;
+        for (int64_t c = 0; c < n; ++c)
+            if (!taken[c]) cands[m++] = (int32_t)c;
+        rc = oracle_gain(V, n, d, S_out, i, cands, m, score, nthreads);
+        if (rc) break;
+        int64_t best = 0;
+        for (int64_t q = 1; q < m; ++q)
+            if (score[q] > score[best]) best = q; /* strict: the lowest index wins ties */
+        S_out[i] = cands[best];
+        f_out[i] = score[best];
+        taken[cands[best]] = 1;
+    }
+    free(cands);
+    free(score);
+    free(taken);
+    return rc;
+}

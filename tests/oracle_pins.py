@@ -11,7 +11,9 @@ disagrees with something fixed independently of it:
 - the loss as a nearest-neighbour query answered by a k-d tree (SciPy), an
   algorithm that shares nothing with the oracle's direct loop;
 - closed forms (one-point ground set, k = 1 through the norm expansion),
-  exact scaling by 2, order invariance, the greedy multiset of Section IV-A.
+  exact scaling by 2, order invariance, the greedy multiset of Section IV-A;
+- Algorithm 1 against a hand-worked run and against the (1 - 1/e) bound of
+  Section III over brute-force optima.
 
 The same battery runs against deliberately broken builds of the oracle
 (tests/test_oracle_mutants.py) to show that each planted mistake trips a pin.
@@ -59,6 +61,10 @@ def pin_worked_examples(o):
     gg = g["gain"]
     got = o.gain(np.array(gg["V"], float), gg["S"], gg["cands"], 1)
     _close(got, [a / b for a, b in gg["value"]], what="greedy multiset")
+    gr = g["greedy"]
+    S, f = o.greedy(np.array(gr["V"], float), gr["K"], 1)
+    assert list(S) == gr["S"], f"greedy order {list(S)}"
+    _close(f, [a / b for a, b in gr["f"]], what="greedy values")
 
 
 def pin_empty_and_full(o):
@@ -205,6 +211,22 @@ def pin_empty_slots(o):
     assert np.array_equal(got, np.asarray(want)), f"blank fields: {got} vs {want}"
 
 
+def pin_greedy_guarantee(o):
+    """Algorithm 1 reaches at least (1 - 1/e) of the best size-K subset
+    (Section III), checked against brute force; each round's value is f of
+    the prefix, and f never decreases."""
+    for seed, (n, d, K) in enumerate([(8, 2, 3), (9, 3, 4), (7, 1, 2)]):
+        V = _rng_points(300 + seed, n, d, 2.0)
+        S, f = o.greedy(V, K, 1)
+        assert len(set(S.tolist())) == K, "greedy repeated a point"
+        for i in range(K):
+            _close([f[i]], o.eval(V, S[None, :i + 1], 1), what="greedy prefix value")
+        assert np.all(np.diff(f) >= -1e-12), "greedy values decrease"
+        combos = np.array(list(itertools.combinations(range(n), K)), np.int32)
+        best = o.eval(V, combos, 1).max()
+        assert f[-1] >= (1 - np.exp(-1)) * best - 1e-12, "greedy below (1 - 1/e) OPT"
+
+
 PINS = [pin_worked_examples, pin_empty_and_full, pin_monotone_submodular_bruteforce,
         pin_kdtree_nearest_neighbour, pin_closed_forms, pin_scaling_and_order,
-        pin_threads_and_gain, pin_invalid_index, pin_empty_slots]
+        pin_threads_and_gain, pin_invalid_index, pin_empty_slots, pin_greedy_guarantee]
