@@ -133,6 +133,33 @@ EXEMCL_API int exemplar_gain(const float *V, int64_t n, int64_t d, const int32_t
                              const int32_t *cands, int64_t l, float *out, void *stream);
 
 /*
+ * exemplar_greedy -- the Greedy optimizer of Algorithm 1, run on the device.
+ *
+ * K rounds; round i scores f(S u {c}) for every point c of V not yet in S
+ * (the same computation as exemplar_gain, with the cache g(v) kept on the
+ * device and updated as g <- max(g, <v,c*> - ||c*||^2/2) after each round),
+ * and adds the best candidate c*.  Ties go to the lowest index (Algorithm 1
+ * leaves the choice open); a NaN score ranks below every number.  The
+ * rounds are queued back to back on the stream: no host synchronisation.
+ *
+ *   V      device, n x d fp32 row-major; read only
+ *   n, d   as for exemplar_eval
+ *   K      rounds, 0 <= K <= n
+ *   S_out  device, K int32; S_out[i] = the point added in round i
+ *   f_out  device, K floats; f_out[i] = f({S_out[0], ..., S_out[i]})
+ *   stream hipStream_t or NULL
+ *
+ * Scores of round i are those exemplar_gain returns for S = S_out[0..i-1]
+ * (bitwise), so f_out[i] - f_out[i-1] is the round's discrete derivative
+ * (Definition 1).  Temporary memory: about 17 bytes per point plus a scoring
+ * workspace kept under 1 GiB by scoring the candidates in chunks.
+ * Errors: EINVAL for bad sizes (K > n, d > 512) or NULL outputs when K > 0;
+ * ENOMEM / EDEVICE as for exemplar_eval.
+ */
+EXEMCL_API int exemplar_greedy(const float *V, int64_t n, int64_t d, int64_t K, int32_t *S_out,
+                               float *f_out, void *stream);
+
+/*
  * exemplar_sqnorm -- q[i] = ||v_i||^2, the squared distance of every ground
  * point to e0, in fp32.  Its mean is L({e0}), the set-independent term of
  * Eq. (4) that the paper computes once up front (Section IV-B, Algorithm).

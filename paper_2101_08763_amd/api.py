@@ -18,7 +18,7 @@ EXEMCL_OK, EXEMCL_EINVAL, EXEMCL_ENOMEM, EXEMCL_EDEVICE = 0, 1, 2, 3
 PATH_NONE, PATH_VALU, PATH_MFMA = 0, 1, 2
 PATH_NAMES = {PATH_NONE: "none", PATH_VALU: "valu", PATH_MFMA: "mfma"}
 
-EXPORTED = ("exemplar_eval", "exemplar_gain", "exemplar_sqnorm", "exemplar_plan",
+EXPORTED = ("exemplar_eval", "exemplar_gain", "exemplar_greedy", "exemplar_sqnorm", "exemplar_plan",
             "exemplar_prof_enable", "exemplar_prof_read", "exemplar_strerror", "exemplar_version")
 
 
@@ -47,6 +47,8 @@ def load(path: str | None = None) -> ctypes.CDLL:
     lib.exemplar_eval.restype = ip
     lib.exemplar_gain.argtypes = [vp, i64, i64, vp, i64, vp, i64, vp, vp]
     lib.exemplar_gain.restype = ip
+    lib.exemplar_greedy.argtypes = [vp, i64, i64, i64, vp, vp, vp]
+    lib.exemplar_greedy.restype = ip
     lib.exemplar_sqnorm.argtypes = [vp, i64, i64, ip, vp, vp]
     lib.exemplar_sqnorm.restype = ip
     lib.exemplar_plan.argtypes = [i64, i64, i64, i64, ip, ctypes.POINTER(ctypes.c_int),
@@ -145,6 +147,30 @@ def exemplar_gain(V, S, cands, out=None, stream=None):
     if rc != EXEMCL_OK:
         raise ExemclError(rc, "exemplar_gain")
     return out
+
+
+def exemplar_greedy(V, K, S_out=None, f_out=None, stream=None):
+    """Algorithm 1 for K rounds on fp32 V: returns (S_out, f_out), the point
+    added in each round and f of the solution after it (see exemplar_greedy
+    in exemcl.h)."""
+    import torch
+    if V.dtype != torch.float32:
+        raise TypeError("exemplar_greedy takes float32 V")
+    if V.dim() != 2:
+        raise ValueError("V must be n x d")
+    n, d = V.shape
+    K = int(K)
+    if S_out is None:
+        S_out = torch.empty(max(K, 0), dtype=torch.int32, device=V.device)
+    if f_out is None:
+        f_out = torch.empty(max(K, 0), dtype=torch.float32, device=V.device)
+    if S_out.dtype != torch.int32 or f_out.dtype != torch.float32 or S_out.numel() < K or f_out.numel() < K:
+        raise ValueError("S_out must be int32 and f_out float32, with K elements each")
+    with torch.cuda.device(_check_device(V, S_out if K > 0 else None, f_out if K > 0 else None)):
+        rc = load().exemplar_greedy(_ptr(V), n, d, K, _ptr(S_out), _ptr(f_out), _stream(stream))
+    if rc != EXEMCL_OK:
+        raise ExemclError(rc, "exemplar_greedy")
+    return S_out, f_out
 
 
 def exemplar_sqnorm(V, out=None, stream=None):

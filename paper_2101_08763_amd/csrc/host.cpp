@@ -318,6 +318,80 @@ EXEMCL_API int exemplar_gain(const float *V, int64_t n, int64_t d, const int32_t
     return run_eval(V, n, d, cands, l, 1, EXEMCL_FP32, gcache, S, k, out, st);
 }
 
+EXEMCL_API int exemplar_greedy(const float *V, int64_t n, int64_t d, int64_t K, int32_t *S_out, float *f_out,
+                               void *stream) {
+    if (!V || n < 1 || n > INT32_MAX || d < 1 || d > INT32_MAX) return EXEMCL_EINVAL;
+    if (K < 0 || K > n) return EXEMCL_EINVAL;
+    if (K > 0 && (!S_out || !f_out)) return EXEMCL_EINVAL;
+    MfmaPlan mp;
+    if (!mfma_plan(EXEMCL_FP32, d, &mp)) return EXEMCL_EINVAL;
+    if (K == 0) return EXEMCL_OK;
+    hipStream_t st = (hipStream_t)stream;
+
+    // State kept on the device across rounds: the candidate list V (all of
+    // it; taken ones are skipped by the argmax), the taken flags, the cache
+    // g(v) double-buffered, the round's scores and one staged tile for the
+    // element just added.
+    const int64_t nb = argmax_blocks(n);
+    const int64_t off_taken = align_up(n * 4, 256);
+    const int64_t off_g0 = align_up(off_taken + n, 256);
+    const int64_t off_g1 = align_up(off_g0 + n * 4, 256);
+    const int64_t off_scores = align_up(off_g1 + n * 4, 256);
+    const int64_t off_ctile = align_up(off_scores + n * 4, 256);
+    const int64_t off_pval = align_up(off_ctile + tile_bytes(mp), 256);
+    const int64_t off_pidx = align_up(off_pval + nb * 4, 256);
+    const int64_t fixed = align_up(off_pidx + nb * 4, 256);
+
+    // Candidates are scored in chunks whose temporary memory stays under a
+    // fixed size (the same halving as for a batch that does not fit).
+    constexpr int64_t kScoringBytes = int64_t(1) << 30;
+    const int64_t limit = workspace_limit();
+    int64_t lc = n;
+    Layout L;
+    Scratch ws;
+    for (;;) {
+        if (!layout_eval(n, d, lc, 1, EXEMCL_FP32, EXEMCL_PATH_MFMA, &L)) return EXEMCL_EINVAL;
+        const bool small = L.bytes <= kScoringBytes || lc <= mp.tile;
+        if (small && fixed + L.bytes <= limit) {
+            const int rc = alloc_scratch(&ws, fixed + L.bytes, st);
+            if (rc == EXEMCL_OK) break;
+            if (rc != EXEMCL_ENOMEM) return rc;
+        }
+        if (lc <= mp.tile) return EXEMCL_ENOMEM;
+        lc = ((lc + 1) / 2 + mp.tile - 1) / mp.tile * mp.tile;
+    }
+    char *base = (char *)ws.ptr;
+    int32_t *cands = (int32_t *)base;
+    uint8_t *taken = (uint8_t *)(base + off_taken);
+    float *g_cur = (float *)(base + off_g0), *g_next = (float *)(base + off_g1);
+    float *scores = (float *)(base + off_scores);
+    void *ctile = base + off_ctile;
+    float *pval = (float *)(base + off_pval);
+    int32_t *pidx = (int32_t *)(base + off_pidx);
+    char *work = base + fixed;
+
+    hipError_t e = launch_greedy_init(cands, taken, g_cur, n, st);
+    for (int64_t i = 0; e == hipSuccess && i < K; ++i) {
+        // f(S u {c}) for every candidate c, from the cache of S (Section
+        // IV-A's greedy multiset, scored as single-member sets).
+        for (int64_t j0 = 0; e == hipSuccess && j0 < n; j0 += lc) {
+            const int64_t lj = n - j0 < lc ? n - j0 : lc;
+            Layout Lj;
+            if (!layout_eval(n, d, lj, 1, EXEMCL_FP32, EXEMCL_PATH_MFMA, &Lj)) return EXEMCL_EINVAL;
+            e = run_chunk(Lj, work, V, n, d, cands + j0, lj, 1, EXEMCL_FP32, g_cur, nullptr, 0, scores + j0, st);
+        }
+        if (e == hipSuccess) e = launch_argmax(scores, taken, n, pval, pidx, S_out + i, f_out + i, st);
+        if (i + 1 == K) break;
+        // g <- max(g, h_{c*}) with c* read from S_out[i] on the device.
+        if (e == hipSuccess) e = launch_pack(EXEMCL_FP32, mp, V, n, (int)d, S_out + i, 1, 1, ctile, st);
+        if (e == hipSuccess)
+            e = launch_mfma(EXEMCL_FP32, MODE_ROWMAX, mp, V, n, (int)d, ctile, 1, 1, 1, g_cur, nullptr, 0, g_next,
+                            st);
+        std::swap(g_cur, g_next);
+    }
+    return status_of(e);
+}
+
 EXEMCL_API int exemplar_sqnorm(const void *V, int64_t n, int64_t d, int precision, float *q, void *stream) {
     if (!V || !q) return EXEMCL_EINVAL;
     if (n < 1 || n > INT32_MAX || d < 1 || d > INT32_MAX) return EXEMCL_EINVAL;

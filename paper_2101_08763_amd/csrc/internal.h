@@ -76,8 +76,9 @@ enum Mode { MODE_SUM = 0, MODE_ROWMAX = 1 };
 
 // partials[(rb * waves + w) * lpad + j] = sum over the rows of wavefront w
 // of row block rb of max(m0(v), max_p (<v, s_jp> - ||s_jp||^2 / 2)); m0 = 0
-// when null.  MODE_ROWMAX instead writes rowmax[v] = max(0, max over all
-// staged columns).
+// when null (fp32 only otherwise).  MODE_ROWMAX (fp32, groups_per_chunk =
+// ngroups) instead writes rowmax[v] = max(m0(v), 0, max over all staged
+// columns); rowmax must not alias m0.
 hipError_t launch_mfma(int prec, int mode, const MfmaPlan &pl, const void *V, int64_t n, int d,
                        const void *tiles, int64_t k, int64_t ngroups, int64_t groups_per_chunk,
                        const float *m0, float *partials, int64_t lpad, float *rowmax, hipStream_t st);
@@ -94,5 +95,17 @@ hipError_t launch_reduce(const float *partials, int64_t G, int64_t lpad, int64_t
                          double *scratch, float *out, hipStream_t st);
 
 hipError_t launch_sqnorm(int prec, const void *V, int64_t n, int d, float *q, hipStream_t st);
+
+// Greedy optimizer state (kernels_greedy.hip): cands[i] = i, taken[i] = 0,
+// g[i] = 0 for i < n.
+hipError_t launch_greedy_init(int32_t *cands, uint8_t *taken, float *g, int64_t n, hipStream_t st);
+
+// Partial-result slots the argmax needs (pval and pidx hold this many).
+int64_t argmax_blocks(int64_t n);
+
+// Best untaken scores[i] (largest, lowest i on ties, NaN last): writes its
+// index to *S_slot and its score to *f_slot, and sets taken[i] = 1.
+hipError_t launch_argmax(const float *scores, uint8_t *taken, int64_t n, float *pval, int32_t *pidx,
+                         int32_t *S_slot, float *f_slot, hipStream_t st);
 
 }  // namespace exemcl

@@ -169,7 +169,8 @@ __device__ __forceinline__ void wait_vmcnt() {
 //   partials[(rb * WAVES + w) * lpad + j] = sum over its rows of
 //   max(m0(v), max_p h_{s_jp}(v)),
 // in a fixed order (its registers, then the K-groups of the MFMA layout).
-// MODE_ROWMAX: rowmax[v] = max(0, max over all staged columns of h_s(v)).
+// MODE_ROWMAX: rowmax[v] = max(m0(v), 0, max over all staged columns of
+// h_s(v)) (m0 = 0 when null); rowmax must not alias m0.
 // ---------------------------------------------------------------------------
 template <typename T, int TILE, int NKB, int NKS_LAST, int RT, int WAVES, int MODE, bool HAS_M0>
 __global__ __launch_bounds__(WAVES * 64) void eval_mfma_kernel(const T *__restrict__ V, int64_t n, int d,
@@ -386,7 +387,7 @@ hipError_t eval_launch_t(const MfmaArgs &x, hipStream_t st) {
 
 template <typename T, int TILE, int NKB, int NKS_LAST, int RT, int WAVES, int MODE>
 hipError_t eval_launch(const MfmaArgs &x, hipStream_t st) {
-    if constexpr (MODE == MODE_SUM && sizeof(T) == 4) {
+    if constexpr (sizeof(T) == 4) {
         if (x.m0) return eval_launch_t<T, TILE, NKB, NKS_LAST, RT, WAVES, MODE, true>(x, st);
     }
     return eval_launch_t<T, TILE, NKB, NKS_LAST, RT, WAVES, MODE, false>(x, st);

@@ -78,6 +78,22 @@ def test_gain_rejects(lib, bad):
     assert rc == api.EXEMCL_EINVAL
 
 
+BAD_GREEDY = [dict(V=None), dict(n=0), dict(n=2**31), dict(d=0), dict(d=513), dict(K=-1), dict(K=101),
+              dict(S=None), dict(f=None)]
+
+
+@pytest.mark.parametrize("bad", BAD_GREEDY, ids=[str(b) for b in BAD_GREEDY])
+def test_greedy_rejects(lib, bad):
+    a = dict(V=FAKE, n=100, d=8, K=5, S=FAKE, f=FAKE)
+    a.update(bad)
+    rc = lib.exemplar_greedy(a["V"], a["n"], a["d"], a["K"], a["S"], a["f"], None)
+    assert rc == api.EXEMCL_EINVAL
+
+
+def test_greedy_zero_rounds_is_a_noop(lib):
+    assert lib.exemplar_greedy(FAKE, 100, 8, 0, None, None, None) == api.EXEMCL_OK
+
+
 def test_sqnorm_rejects(lib):
     assert lib.exemplar_sqnorm(None, 10, 2, 0, FAKE, None) == api.EXEMCL_EINVAL
     assert lib.exemplar_sqnorm(FAKE, 10, 2, 0, None, None) == api.EXEMCL_EINVAL
@@ -91,6 +107,8 @@ def test_workspace_limit_gives_enomem(lib, monkeypatch):
     rc = lib.exemplar_eval(FAKE, 100000, 32, FAKE, 256, 10, 0, FAKE, None)
     assert rc == api.EXEMCL_ENOMEM
     rc = lib.exemplar_gain(FAKE, 100000, 32, FAKE, 5, FAKE, 256, FAKE, None)
+    assert rc == api.EXEMCL_ENOMEM
+    rc = lib.exemplar_greedy(FAKE, 100000, 32, 5, FAKE, FAKE, None)
     assert rc == api.EXEMCL_ENOMEM
 
 
