@@ -175,6 +175,84 @@ def copy_probe(steps: int):
     print(json.dumps({"copy_probe_bytes": COPY_PROBE_BYTES, "launches": steps}))
 
 
+def run_paper_sweep(args, dev):
+    """The three series of Section V-A (d = 100; n, l or k varied over 15
+    values with the others at 50 000 / 5 000 / 10), each point timed as
+    --sweep-reps separate exemplar_eval calls (median, min, max), next to the
+    oracle's rate on the host.  One JSON line per (point, precision) on
+    stdout and in --sweep-out; a Markdown table on stderr at the end."""
+    import torch
+
+    axes = ["n", "l", "k"] if args.sweep == "all" else args.sweep.split(",")
+    precs = args.sweep_precisions.split(",")
+    pts = [(a, pt) for a in axes for pt in synth.paper_sweep(a)]
+    log(f"paper sweep: {len(pts)} points x {precs}; drawing {max(pt['n'] for _, pt in pts)} points")
+    Xbig = synth.paper_sweep_points(max(pt["n"] for _, pt in pts))
+    stream = torch.cuda.current_stream()
+    sink = open(args.sweep_out, "w") if args.sweep_out else None
+    table = []
+    for axis, pt in pts:
+        n, l, k = pt["n"], pt["l"], pt["k"]
+        p = synth.paper_sweep_problem(n, l, k, X=Xbig)
+        sets = torch.from_numpy(p.sets).to(dev)
+        cpu = None
+        if not args.no_cpu_baseline:
+            cpu = cpu_baseline(p, p.X.astype(np.float64), args.sweep_cpu_budget)
+        for prec in precs:
+            Xs, _ = synth.rounded(p.X, prec)
+            V = (Xs if isinstance(Xs, torch.Tensor) else torch.from_numpy(Xs)).to(dev).contiguous()
+            out = torch.empty(l, dtype=torch.float32, device=dev)
+            for _ in range(2):
+                api.exemplar_eval(V, sets, out=out)
+            torch.cuda.synchronize()
+            api.exemplar_prof_read()
+            api.exemplar_prof_enable(True)
+            evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                   for _ in range(args.sweep_reps)]
+            for a, b in evs:
+                a.record(stream)
+                api.exemplar_eval(V, sets, out=out)
+                b.record(stream)
+            torch.cuda.synchronize()
+            api.exemplar_prof_enable(False)
+            kern_ms, launches = api.exemplar_prof_read()
+            times = [a.elapsed_time(b) for a, b in evs]
+            med = statistics.median(times)
+            kern = kern_ms / max(launches, 1)
+            flops = 2.0 * n * l * k * synth.PAPER_SWEEP_D
+            rec = {
+                "series": axis, "n": n, "l": l, "k": k, "d": synth.PAPER_SWEEP_D, "precision": prec,
+                "reps": args.sweep_reps, "ms_median": med, "ms_min": min(times), "ms_max": max(times),
+                "set_evals_per_s": l / (med * 1e-3), "kernel_ms": kern,
+                "kernel_tflops": flops / (kern * 1e-3) / 1e12,
+                "kernel_frac": flops / (kern * 1e-3) / 1e12 / PEAK_TFLOPS[prec],
+            }
+            if cpu is not None:
+                rec["oracle_set_evals_per_s"] = cpu["value"]
+                rec["oracle_threads"] = cpu["cores"]
+                rec["speedup_vs_oracle"] = rec["set_evals_per_s"] / cpu["value"]
+            line = json.dumps(rec)
+            print(line, flush=True)
+            if sink:
+                sink.write(line + "\n")
+                sink.flush()
+            table.append(rec)
+            log(f"{axis}: n={n} l={l} k={k} {prec}: {med:.3f} ms median, kernel {rec['kernel_tflops']:.1f} TFLOP/s "
+                f"({100 * rec['kernel_frac']:.1f} %)" + (f", x{rec['speedup_vs_oracle']:.0f} vs oracle" if cpu else ""))
+            del V, out
+        del sets
+    if sink:
+        sink.close()
+    log("| series | n | l | k | precision | median ms | min ms | max ms | set evals/s | kernel TFLOP/s | "
+        "% peak | oracle set evals/s | speedup |")
+    log("|---|---|---|---|---|---|---|---|---|---|---|---|---|")
+    for r in table:
+        o = r.get("oracle_set_evals_per_s")
+        log(f"| {r['series']} | {r['n']} | {r['l']} | {r['k']} | {r['precision']} | {r['ms_median']:.3f} | "
+            f"{r['ms_min']:.3f} | {r['ms_max']:.3f} | {r['set_evals_per_s']:.3g} | {r['kernel_tflops']:.1f} | "
+            f"{100 * r['kernel_frac']:.1f} | " + (f"{o:.3g} | {r['speedup_vs_oracle']:.0f} |" if o else "- | - |"))
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -187,6 +265,12 @@ def main():
     ap.add_argument("--traffic-summary", metavar="DIR",
                     help="summarise rocprofv3 FETCH_SIZE/WRITE_SIZE runs under DIR into profiles/")
     ap.add_argument("--kernel", default="eval_mfma_kernel", help="kernel name for --traffic-summary")
+    ap.add_argument("--sweep", metavar="SERIES",
+                    help="run the Section V-A series instead: n, l, k (comma-separated) or all")
+    ap.add_argument("--sweep-precisions", default="fp32,fp16")
+    ap.add_argument("--sweep-reps", type=int, default=15, help="timed calls per sweep point (median reported)")
+    ap.add_argument("--sweep-out", metavar="FILE", help="also write the sweep's JSON lines to FILE")
+    ap.add_argument("--sweep-cpu-budget", type=float, default=1.0, help="seconds of oracle time per sweep point")
     args = ap.parse_args()
 
     if args.traffic_summary:
@@ -208,6 +292,9 @@ def main():
         copy_probe(max(args.steps, 1))
         return
     api.load()
+    if args.sweep:
+        run_paper_sweep(args, dev)
+        return
 
     w = synth.WORKLOADS[args.workload]
     log(f"generating {w.name}: {w.note}")

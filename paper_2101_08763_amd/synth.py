@@ -11,7 +11,8 @@ Draw order for every workload (NumPy PCG64, ``numpy.random.default_rng(seed)``):
 2. cluster labels, shape (n,): ``integers(0, C)``;
 3. points: ``means[labels] + standard_normal((n, d))`` (sigma = 1);
    i.i.d. workloads skip steps 1-2 and use ``standard_normal((n, d))``;
-4. sets: one ``choice(n, k, replace=False)`` per set, in set order.
+4. sets: one ``choice(n, k, replace=False)`` per set, in set order (the
+   paper-shaped sweep below draws its larger batches differently).
    Greedy workloads draw the base set S with ``choice(n, |S|)`` and then
    ``choice(n, l + |S|)`` candidates, drop the ones in S and keep the first l.
 
@@ -138,3 +139,72 @@ def rounded(X: np.ndarray, precision: str):
         Xs = torch.from_numpy(np.ascontiguousarray(X, dtype=np.float32)).to(torch.bfloat16)
         return Xs, Xs.to(torch.float64).numpy()
     raise ValueError(f"unknown precision {precision!r}")
+
+
+# ---------------------------------------------------------------------------
+# The scaling experiment of Section V-A: d = 100, a default problem of
+# n = 50 000 points, l = 5 000 sets, k = 10 members, and three series that
+# vary one of n, l, k over 15 uniformly spaced values of an interval while the
+# other two keep their defaults.  The paper states no distribution; points
+# are i.i.d. N(0, 1) here, ``default_rng(seed).standard_normal((n, 100))``
+# (so every n of the series is a prefix of the largest array).  Sets come
+# from ``default_rng(seed + 1)``: ``integers(0, n, (l, k))``, then, for the
+# rows that still hold a repeat (in row order), every member equal to an
+# earlier one of its row (ranked by a stable sort of the row) is redrawn with
+# ``integers(0, n)`` in row-major order, until every row holds k distinct
+# points.
+# ---------------------------------------------------------------------------
+PAPER_SWEEP_D = 100
+PAPER_SWEEP_DEFAULT = {"n": 50_000, "l": 5_000, "k": 10}
+PAPER_SWEEP_RANGE = {"n": (1_000, 400_000), "l": (1_000, 40_000), "k": (10, 500)}
+PAPER_SWEEP_POINTS = 15
+PAPER_SWEEP_SEED = 5
+
+
+def paper_sweep(axis: str) -> list[dict]:
+    """The 15 (n, l, k) points of one series of Section V-A."""
+    lo, hi = PAPER_SWEEP_RANGE[axis]
+    out = []
+    for v in np.linspace(lo, hi, PAPER_SWEEP_POINTS):
+        pt = dict(PAPER_SWEEP_DEFAULT)
+        pt[axis] = int(round(float(v)))
+        out.append(pt)
+    return out
+
+
+def draw_sets_redraw(rng: np.random.Generator, n: int, l: int, k: int) -> np.ndarray:
+    if k > n:
+        raise ValueError("k distinct members need k <= n")
+    sets = rng.integers(0, n, size=(l, k), dtype=np.int64)
+    rows = np.arange(l)
+    while rows.size:
+        sub = sets[rows]
+        order = np.argsort(sub, axis=1, kind="stable")
+        srt = np.take_along_axis(sub, order, axis=1)
+        rep_sorted = np.zeros(srt.shape, dtype=bool)
+        rep_sorted[:, 1:] = srt[:, 1:] == srt[:, :-1]
+        bad = rep_sorted.any(axis=1)
+        if not bad.any():
+            break
+        rep = np.zeros_like(rep_sorted)
+        np.put_along_axis(rep, order, rep_sorted, axis=1)
+        sub[rep] = rng.integers(0, n, size=int(rep.sum()))
+        sets[rows] = sub
+        rows = rows[bad]
+    return np.ascontiguousarray(sets, dtype=np.int32)
+
+
+def paper_sweep_points(n: int, seed: int = PAPER_SWEEP_SEED) -> np.ndarray:
+    return np.random.default_rng(seed).standard_normal((n, PAPER_SWEEP_D), dtype=np.float32)
+
+
+def paper_sweep_problem(n: int, l: int, k: int, seed: int = PAPER_SWEEP_SEED,
+                        X: np.ndarray | None = None) -> Problem:
+    """One point of the series; ``X`` may be the points of a larger n of the
+    same seed (its first n rows are used)."""
+    X = paper_sweep_points(n, seed) if X is None else np.ascontiguousarray(X[:n])
+    if X.shape != (n, PAPER_SWEEP_D):
+        raise ValueError("X holds fewer than n points")
+    w = Workload(f"paper_n{n}_l{l}_k{k}", n, PAPER_SWEEP_D, l, k, 0, seed, "fp32", "eval",
+                 f"{n} points, d=100, i.i.d. N(0,1); {l} sets of {k} (Section V-A series)")
+    return Problem(w, X, sets=draw_sets_redraw(np.random.default_rng(seed + 1), n, l, k))

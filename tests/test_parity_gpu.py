@@ -153,6 +153,23 @@ def test_sweep_sampled(torch_gpu, orc, d, prec):
     assert np.all(np.isfinite(got)) and np.all(got >= 0)
 
 
+@pytest.mark.parametrize("prec", ["fp32", "fp16"])
+@pytest.mark.parametrize("axis", ["n", "l", "k"])
+def test_paper_sweep_sampled(torch_gpu, orc, axis, prec):
+    """Section V-A series: the second point (ragged sizes) and the largest
+    of each series, every set on the GPU, a strided sample on the oracle."""
+    torch = torch_gpu
+    pts = synth.paper_sweep(axis)
+    for pt in (pts[1], pts[-1]):
+        p = synth.paper_sweep_problem(pt["n"], pt["l"], pt["k"])
+        say(f"  series {axis}: n={pt['n']} l={pt['l']} k={pt['k']} {prec}")
+        Vg, X64 = to_gpu(torch, p.X, prec)
+        got = gpu_eval(torch, Vg, p.sets)
+        assert np.all(np.isfinite(got))
+        idx = strided(pt["l"], 12)
+        check(got[idx], orc.eval(X64, p.sets[idx]), orc.loss_e0(X64), prec, f"series {axis} {pt}")
+
+
 def test_greedy200k_sampled(torch_gpu, orc):
     p = synth.make("greedy200k")
     say("greedy200k: 200 000 x 100 fp32, |S|=19, 4096 candidates")
