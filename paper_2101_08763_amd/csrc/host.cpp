@@ -59,7 +59,7 @@ struct Layout {
     MfmaPlan mp{};
     ValuPlan vp{};
     int64_t G = 0, lpad = 0, ngroups = 0, gpc = 0;
-    int64_t off_partials = 0, off_tiles = 0, off_aux = 0, bytes = 0;
+    int64_t off_partials = 0, off_tiles = 0, bytes = 0;
 };
 
 int64_t tile_bytes(const MfmaPlan &mp) { return mfma_tile_bytes(mp); }
@@ -83,8 +83,7 @@ bool layout_eval(int64_t n, int64_t d, int64_t l, int64_t k, int precision, int 
         L->gpc = (L->ngroups + chunks - 1) / chunks;
         L->off_partials = 0;
         L->off_tiles = align_up(L->G * L->lpad * 4, 256);
-        L->off_aux = align_up(L->off_tiles + L->ngroups * k * tile_bytes(L->mp), 256);
-        L->bytes = align_up(L->off_aux + reduce_scratch_bytes(L->G, l), 256);
+        L->bytes = align_up(L->off_tiles + L->ngroups * k * tile_bytes(L->mp), 256);
         return true;
     }
     if (path == EXEMCL_PATH_VALU) {
@@ -92,8 +91,7 @@ bool layout_eval(int64_t n, int64_t d, int64_t l, int64_t k, int precision, int 
         L->lpad = l;
         L->G = (n + L->vp.rows - 1) / L->vp.rows;
         L->off_partials = 0;
-        L->off_aux = align_up(L->G * L->lpad * 4, 256);
-        L->bytes = align_up(L->off_aux + reduce_scratch_bytes(L->G, l), 256);
+        L->bytes = align_up(L->G * L->lpad * 4, 256);
         return true;
     }
     L->bytes = 0;
@@ -205,6 +203,7 @@ struct ProfRange {
 hipError_t run_chunk(const Layout &L, char *base, const void *V, int64_t n, int64_t d, const int32_t *sets,
                      int64_t l, int64_t k, int precision, const float *m0, const int32_t *common, int64_t kcommon,
                      float *out, hipStream_t st) {
+    if (L.path == EXEMCL_PATH_NONE) return launch_zero(out, l, st);  // k = 0: every set is empty
     float *partials = (float *)(base + L.off_partials);
     hipError_t e = hipSuccess;
     if (L.path == EXEMCL_PATH_MFMA) {
@@ -222,8 +221,7 @@ hipError_t run_chunk(const Layout &L, char *base, const void *V, int64_t n, int6
         pr.end();
     }
     if (e == hipSuccess)
-        e = launch_reduce(partials, L.G, L.lpad, l, n, sets, k, common, kcommon, (double *)(base + L.off_aux), out,
-                          st);
+        e = launch_reduce(partials, L.G, L.lpad, l, n, sets, k, common, kcommon, out, st);
     return e;
 }
 

@@ -87,14 +87,16 @@ hipError_t launch_valu(int prec, const ValuPlan &pl, const void *V, int64_t n, i
                        int64_t l, int64_t k, float *partials, int64_t lpad, hipStream_t st);
 
 // out[j] = (2/n) * sum_g partials[g * lpad + j] (fp64, fixed order), or NaN
-// when an index of set j (or of the common list) is outside [0, n).
-// `scratch` holds reduce_scratch_bytes(G, l) bytes.
-int64_t reduce_scratch_bytes(int64_t G, int64_t l);
+// when an index of set j (or of the common list) is outside [0, n) and not
+// the empty slot.
 hipError_t launch_reduce(const float *partials, int64_t G, int64_t lpad, int64_t l, int64_t n,
-                         const int32_t *sets, int64_t kset, const int32_t *common, int64_t kcommon,
-                         double *scratch, float *out, hipStream_t st);
+                         const int32_t *sets, int64_t kset, const int32_t *common, int64_t kcommon, float *out,
+                         hipStream_t st);
 
 hipError_t launch_sqnorm(int prec, const void *V, int64_t n, int d, float *q, hipStream_t st);
+
+// out[i] = 0 for i < count (f of empty sets).
+hipError_t launch_zero(float *out, int64_t count, hipStream_t st);
 
 // Greedy optimizer state (kernels_greedy.hip): cands[i] = i, taken[i] = 0,
 // g[i] = 0 for i < n.

@@ -1,5 +1,5 @@
 // kernels_aux.hip -- vector-ALU evaluation for small d, the fixed-order
-// reduction of partial sums, squared norms and a fill kernel.
+// reduction of partial sums and squared norms.
 #include <float.h>
 #include <math.h>
 
@@ -156,40 +156,54 @@ hipError_t launch_valu(int prec, const ValuPlan &pl, const void *V, int64_t n, i
 }
 
 // ---------------------------------------------------------------------------
-// Second pass: out[j] = (2/n) * sum_g partials[g][j].
+// Second pass: out[j] = (2/n) * sum_g partials[g][j], fp64, one launch.
 //
-// Stage 1: the G partial rows are cut into chunks of rchunk(G) consecutive
-// rows; thread (j, c) adds chunk c of column j in fp64, in row order.  Stage 2 adds
-// the chunk sums of column j in chunk order.  The chunking depends on G only,
-// so the summation order of a set does not depend on the batch.  The index
-// check turns a set with an index outside [0, n) into NaN.
+// A workgroup owns RJ sets and all G partial rows; its threads are RQ row
+// lanes x RJ sets (consecutive threads read consecutive sets of one row).
+// Row lane q adds rows q, q + RQ, q + 2 RQ, ... in order; the RQ lane sums
+// are then added by a fixed pairwise tree.  The order depends on G only, so
+// the result of a set does not depend on the batch it is in.  The index
+// check turns a set with an index outside [0, n) other than the empty slot
+// into NaN.
 // ---------------------------------------------------------------------------
-static int64_t rchunk(int64_t G) {
-    const int64_t c = (G + 65534) / 65535;  // keeps the chunk count within grid.y
-    return c > 32 ? c : 32;
-}
+constexpr int RJ = 16;
+constexpr int RQ = 64;
 
-__global__ __launch_bounds__(256) void reduce_chunks_kernel(const float *__restrict__ partials, int64_t G,
-                                                            int64_t lpad, int64_t l, int64_t rows_per_chunk,
-                                                            double *__restrict__ chunks) {
-    const int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x;
-    const int64_t c = blockIdx.y;
-    if (j >= l) return;
-    const int64_t g0 = c * rows_per_chunk;
-    const int64_t g1 = min(G, g0 + rows_per_chunk);
-    double s = 0.0;
-    for (int64_t g = g0; g < g1; ++g) s += (double)partials[g * lpad + j];
-    chunks[c * l + j] = s;
-}
+__global__ __launch_bounds__(RJ * RQ) void reduce_sets_kernel(const float *__restrict__ partials, int64_t G,
+                                                              int64_t lpad, int64_t l, int64_t n,
+                                                              const int32_t *__restrict__ sets, int64_t kset,
+                                                              const int32_t *__restrict__ common, int64_t kcommon,
+                                                              float *__restrict__ out) {
+    __shared__ double part[RQ][RJ];
+    const int tid = threadIdx.x;
+    const int jl = tid % RJ, q = tid / RJ;
+    const int64_t j = (int64_t)blockIdx.x * RJ + jl;
 
-__global__ __launch_bounds__(256) void reduce_final_kernel(const double *__restrict__ chunks, int64_t nchunks,
-                                                           int64_t l, int64_t n, const int32_t *__restrict__ sets,
-                                                           int64_t kset, const int32_t *__restrict__ common,
-                                                           int64_t kcommon, float *__restrict__ out) {
-    const int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x;
-    if (j >= l) return;
-    double s = 0.0;
-    for (int64_t c = 0; c < nchunks; ++c) s += chunks[c * l + j];
+    // Loads are issued UNR at a time (rows past G re-read row G-1 and are
+    // then replaced by +0.0, which changes no sum), so the additions still
+    // run in row order.
+    constexpr int UNR = 8;
+    double acc = 0.0;
+    if (j < l) {
+        for (int64_t g = q; g < G; g += RQ * UNR) {
+            float x[UNR];
+#pragma unroll
+            for (int u = 0; u < UNR; ++u) x[u] = partials[min(g + u * RQ, G - 1) * lpad + j];
+#pragma unroll
+            for (int u = 0; u < UNR; ++u)
+                if (g + u * RQ >= G) x[u] = 0.0f;
+#pragma unroll
+            for (int u = 0; u < UNR; ++u) acc += (double)x[u];
+        }
+    }
+    part[q][jl] = acc;
+    __syncthreads();
+#pragma unroll
+    for (int w = RQ / 2; w >= 1; w >>= 1) {
+        if (q < w) part[q][jl] += part[q + w][jl];
+        __syncthreads();
+    }
+    if (q != 0 || j >= l) return;
     bool bad = false;
     for (int64_t p = 0; p < kset; ++p) {
         const int64_t idx = sets[j * kset + p];
@@ -199,27 +213,27 @@ __global__ __launch_bounds__(256) void reduce_final_kernel(const double *__restr
         const int64_t idx = common[p];
         bad |= idx != kEmptySlot && (idx < 0 || idx >= n);
     }
-    out[j] = bad ? __builtin_nanf("") : (float)(2.0 * s / (double)n);
-}
-
-int64_t reduce_scratch_bytes(int64_t G, int64_t l) {
-    return ((G + rchunk(G) - 1) / rchunk(G)) * l * (int64_t)sizeof(double);
+    out[j] = bad ? __builtin_nanf("") : (float)(2.0 * part[0][jl] / (double)n);
 }
 
 hipError_t launch_reduce(const float *partials, int64_t G, int64_t lpad, int64_t l, int64_t n,
-                         const int32_t *sets, int64_t kset, const int32_t *common, int64_t kcommon, double *scratch,
-                         float *out, hipStream_t st) {
-    const int64_t blocks = (l + 255) / 256;
-    const int64_t rc = rchunk(G);
-    const int64_t nchunks = (G + rc - 1) / rc;
-    if (nchunks > 0) {
-        hipLaunchKernelGGL(reduce_chunks_kernel, dim3((unsigned)blocks, (unsigned)nchunks), dim3(256), 0, st,
-                           partials, G, lpad, l, rc, scratch);
-        hipError_t e = hipGetLastError();
-        if (e != hipSuccess) return e;
-    }
-    hipLaunchKernelGGL(reduce_final_kernel, dim3((unsigned)blocks), dim3(256), 0, st, scratch, nchunks, l, n, sets,
-                       kset, common, kcommon, out);
+                         const int32_t *sets, int64_t kset, const int32_t *common, int64_t kcommon, float *out,
+                         hipStream_t st) {
+    if (l == 0) return hipSuccess;
+    hipLaunchKernelGGL(reduce_sets_kernel, dim3((unsigned)((l + RJ - 1) / RJ)), dim3(RJ * RQ), 0, st, partials, G,
+                       lpad, l, n, sets, kset, common, kcommon, out);
+    return hipGetLastError();
+}
+
+// f of empty sets (k = 0): out[j] = 0, e0 alone.
+__global__ __launch_bounds__(256) void zero_kernel(float *__restrict__ out, int64_t count) {
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i < count) out[i] = 0.0f;
+}
+
+hipError_t launch_zero(float *out, int64_t count, hipStream_t st) {
+    if (count == 0) return hipSuccess;
+    hipLaunchKernelGGL(zero_kernel, dim3((unsigned)((count + 255) / 256)), dim3(256), 0, st, out, count);
     return hipGetLastError();
 }
 

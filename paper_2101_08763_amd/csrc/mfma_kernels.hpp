@@ -50,9 +50,11 @@ constexpr int tile_bytes_of() {
 // Byte layout of one tile (HDR + nkb * 1024 bytes):
 //   [0, HDR)               TM fp32 biases -||s||^2/2, one per column
 //   [HDR + kb*1024 + 16*L)  lane L's 16-byte B-operand vector for k-block kb
-// Padding columns (set >= l) and invalid indices become zero vectors with
-// bias -FLT_MAX, which never wins the running max.  Coordinates past d are
-// zero.  One wavefront per tile.
+// Padding columns (set >= l), empty slots and invalid indices become zero
+// vectors with bias -FLT_MAX, which never wins the running max.
+// Coordinates past d are zero.  One wavefront per tile; ||s||^2 is summed
+// from the lane vectors (fp32, k-blocks then elements in order, then the
+// K-groups of the column with a fixed xor tree).
 // ---------------------------------------------------------------------------
 template <typename T, int TILE>
 __global__ __launch_bounds__(64) void pack_tiles_kernel(const T *__restrict__ V, int64_t n, int d,
@@ -70,20 +72,19 @@ __global__ __launch_bounds__(64) void pack_tiles_kernel(const T *__restrict__ V,
     const bool valid = idx >= 0 && idx < n;
     unsigned char *tile = tiles + t * (int64_t)(HDR + nkb * 1024);
     typename M::vec_t *dst = reinterpret_cast<typename M::vec_t *>(tile + HDR);
+    float q = 0.0f;
     for (int kb = 0; kb < nkb; ++kb) {
-        dst[kb * 64 + lane] = load_lanevec<M>(V, n, d, valid ? idx : n, kb, grp, vec_ok);
-    }
-    if (grp == 0) {
-        float q = 0.0f;
-        if (valid) {
-            const T *row = V + idx * (int64_t)d;
-            for (int e = 0; e < d; ++e) {
-                const float x = to_f32(row[e]);
-                q = fmaf(x, x, q);
-            }
+        const typename M::vec_t v = load_lanevec<M>(V, n, d, valid ? idx : n, kb, grp, vec_ok);
+        dst[kb * 64 + lane] = v;
+#pragma unroll
+        for (int e = 0; e < M::VEC; ++e) {
+            const float x = to_f32(v[e]);
+            q = fmaf(x, x, q);
         }
-        reinterpret_cast<float *>(tile)[col] = valid ? -0.5f * q : -FLT_MAX;
     }
+#pragma unroll
+    for (int off = M::TM; off < 64; off <<= 1) q += __shfl_xor(q, off);
+    if (grp == 0) reinterpret_cast<float *>(tile)[col] = valid ? -0.5f * q : -FLT_MAX;
 }
 
 // Stage geometry, fixed at compile time per k-block bucket.  Workgroups of
