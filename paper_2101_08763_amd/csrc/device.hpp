@@ -29,55 +29,59 @@ __device__ __forceinline__ float to_f32(__bf16 x) { return (float)x; }
 //   GROUPS  64 / TM lane groups; lane L holds A row / output column L % TM and
 //           belongs to K-group L / TM
 //   VEC     storage elements per 16-byte lane vector
-//   KPL     K elements one lane feeds into one instruction
 //   KS_PER_KB  instructions fed by one 16-byte lane vector (a "k-block")
 //   KB_DIMS    coordinates covered by one k-block across the wavefront
 //   ACC     fp32 accumulators per lane
 //
 // Coordinate of lane-vector element e, for a lane in K-group `grp`, inside
-// k-block kb: dim(kb, grp, e).  A (rows) and B (exemplars) use the same map,
-// so each instruction pairs matching coordinates; which K slot of the
-// instruction a coordinate lands in only changes the summation order.
+// k-block kb: dim(kb, grp, e) = kb*KB_DIMS + grp*VEC + e, so every lane
+// vector is VEC consecutive coordinates of one row (one 16-byte load).  A
+// (rows) and B (exemplars) use the same map, so each instruction pairs
+// matching coordinates; which K slot of the instruction a coordinate lands
+// in only changes the summation order.
 template <typename T, int TILE>
 struct Mfma;
 
 // fp32: v_mfma_f32_32x32x2_f32.  Element e of the lane vector feeds
-// instruction e of the k-block; instruction e covers coordinates
-// kb*8 + 2e + {0,1}, so a ragged d wastes at most one coordinate.
+// instruction e of the k-block, which covers coordinates kb*8 + {e, 4 + e}.
 template <>
 struct Mfma<float, 32> {
-    static constexpr int TM = 32, GROUPS = 2, VEC = 4, KPL = 1;
-    static constexpr int KS_PER_KB = 4, KB_DIMS = 8, ACC = 16, KSTEP = 2;
+    static constexpr int TM = 32, GROUPS = 2, VEC = 4;
+    static constexpr int KS_PER_KB = 4, KB_DIMS = 8, ACC = 16;
     using acc_t = f32x16;
     using vec_t = f32x4;
-    __device__ __forceinline__ static int dim(int kb, int grp, int e) { return kb * KB_DIMS + e * GROUPS + grp; }
+    using elem_t = float;
+    __device__ __forceinline__ static int dim(int kb, int grp, int e) { return kb * KB_DIMS + grp * VEC + e; }
     __device__ __forceinline__ static acc_t mma(vec_t a, vec_t b, int e, acc_t c) {
         return __builtin_amdgcn_mfma_f32_32x32x2f32(a[e], b[e], c, 0, 0, 0);
     }
 };
 
 // fp32: v_mfma_f32_16x16x4_f32 (16 rows per tile: half the A registers of the
-// 32x32 shape per row, used for large d).
+// 32x32 shape per row, used for large d).  Instruction e covers coordinates
+// kb*16 + {e, 4 + e, 8 + e, 12 + e}.
 template <>
 struct Mfma<float, 16> {
-    static constexpr int TM = 16, GROUPS = 4, VEC = 4, KPL = 1;
-    static constexpr int KS_PER_KB = 4, KB_DIMS = 16, ACC = 4, KSTEP = 4;
+    static constexpr int TM = 16, GROUPS = 4, VEC = 4;
+    static constexpr int KS_PER_KB = 4, KB_DIMS = 16, ACC = 4;
     using acc_t = f32x4;
     using vec_t = f32x4;
-    __device__ __forceinline__ static int dim(int kb, int grp, int e) { return kb * KB_DIMS + e * GROUPS + grp; }
+    using elem_t = float;
+    __device__ __forceinline__ static int dim(int kb, int grp, int e) { return kb * KB_DIMS + grp * VEC + e; }
     __device__ __forceinline__ static acc_t mma(vec_t a, vec_t b, int e, acc_t c) {
         return __builtin_amdgcn_mfma_f32_16x16x4f32(a[e], b[e], c, 0, 0, 0);
     }
 };
 
 // fp16: v_mfma_f32_32x32x16_f16 (gfx950).  One lane vector = the 8 K
-// elements of one instruction; coordinates kb*16 + grp*8 + e.
+// elements of one instruction.
 template <>
 struct Mfma<_Float16, 32> {
-    static constexpr int TM = 32, GROUPS = 2, VEC = 8, KPL = 8;
-    static constexpr int KS_PER_KB = 1, KB_DIMS = 16, ACC = 16, KSTEP = 16;
+    static constexpr int TM = 32, GROUPS = 2, VEC = 8;
+    static constexpr int KS_PER_KB = 1, KB_DIMS = 16, ACC = 16;
     using acc_t = f32x16;
     using vec_t = f16x8;
+    using elem_t = _Float16;
     __device__ __forceinline__ static int dim(int kb, int grp, int e) { return kb * KB_DIMS + grp * VEC + e; }
     __device__ __forceinline__ static acc_t mma(vec_t a, vec_t b, int, acc_t c) {
         return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
@@ -87,10 +91,11 @@ struct Mfma<_Float16, 32> {
 // bf16: v_mfma_f32_32x32x16_bf16 (gfx950), same layout as fp16.
 template <>
 struct Mfma<__bf16, 32> {
-    static constexpr int TM = 32, GROUPS = 2, VEC = 8, KPL = 8;
-    static constexpr int KS_PER_KB = 1, KB_DIMS = 16, ACC = 16, KSTEP = 16;
+    static constexpr int TM = 32, GROUPS = 2, VEC = 8;
+    static constexpr int KS_PER_KB = 1, KB_DIMS = 16, ACC = 16;
     using acc_t = f32x16;
     using vec_t = bf16x8;
+    using elem_t = __bf16;
     __device__ __forceinline__ static int dim(int kb, int grp, int e) { return kb * KB_DIMS + grp * VEC + e; }
     __device__ __forceinline__ static acc_t mma(vec_t a, vec_t b, int, acc_t c) {
         return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
@@ -106,33 +111,44 @@ __device__ __forceinline__ int out_row(int i, int grp) {
     return (i >> 2) * (4 * GROUPS) + 4 * grp + (i & 3);
 }
 
-// Number of MFMA instructions needed to cover d coordinates.
-template <typename M>
-__host__ __device__ constexpr int ksteps_for(int d) {
-    return M::KPL == 1 ? (d + M::GROUPS - 1) / M::GROUPS : (d + M::KB_DIMS - 1) / M::KB_DIMS;
+// Lane vector of row `r` for k-block kb in MFMA operand order; coordinates
+// >= d and rows >= n read as zero.
+//
+// When rows are 16-byte aligned and hold whole lane vectors (`vec_ok`), a
+// vector is either entirely inside the row or entirely past d:
+// lanevec_raw loads it from a clamped, always in-bounds address and
+// lanevec_live says whether to keep it.  Callers issue every raw load of a
+// batch first and select afterwards, so the loads are in flight together.
+template <typename M, typename T>
+__device__ __forceinline__ typename M::vec_t lanevec_raw(const T *__restrict__ V, int64_t n, int d, int64_t r,
+                                                         int kb, int grp) {
+    const int d0 = M::dim(kb, grp, 0);
+    const bool live = r < n && d0 < d;
+    return *reinterpret_cast<const typename M::vec_t *>(V + (live ? r : 0) * (int64_t)d + (live ? d0 : 0));
 }
 
-// Load the lane vector of row `r` for k-block kb in MFMA operand order;
-// coordinates >= d and rows >= n read as zero.  `vec_ok` says rows are
-// 16-byte aligned so a contiguous vector can be fetched in one load.
+template <typename M>
+__device__ __forceinline__ bool lanevec_live(int64_t n, int d, int64_t r, int kb, int grp) {
+    return r < n && M::dim(kb, grp, 0) < d;
+}
+
+template <typename M>
+__device__ __forceinline__ typename M::vec_t lanevec_keep(typename M::vec_t v, bool live) {
+    typename M::vec_t z;
+    for (int e = 0; e < M::VEC; ++e) z[e] = live ? v[e] : (typename M::elem_t)0.0f;
+    return z;
+}
+
+// Element-wise load for rows that are not whole aligned lane vectors.
 template <typename M, typename T>
-__device__ __forceinline__ typename M::vec_t load_lanevec(const T *__restrict__ V, int64_t n, int d, int64_t r,
-                                                          int kb, int grp, bool vec_ok) {
+__device__ __forceinline__ typename M::vec_t lanevec_scalar(const T *__restrict__ V, int64_t n, int d, int64_t r,
+                                                            int kb, int grp) {
     typename M::vec_t v;
-    if (r >= n) {
-        for (int e = 0; e < M::VEC; ++e) v[e] = (T)0.0f;
-        return v;
-    }
-    const T *row = V + r * (int64_t)d;
-    if constexpr (M::KPL > 1) {
-        const int d0 = M::dim(kb, grp, 0);
-        if (vec_ok && d0 + M::VEC <= d) {
-            return *reinterpret_cast<const typename M::vec_t *>(row + d0);
-        }
-    }
+    const int d0 = M::dim(kb, grp, 0);
+    const T *row = V + (r < n ? r : 0) * (int64_t)d;
     for (int e = 0; e < M::VEC; ++e) {
-        const int t = M::dim(kb, grp, e);
-        v[e] = t < d ? row[t] : (T)0.0f;
+        const int t = d0 + e;
+        v[e] = (r < n && t < d) ? row[t] : (T)0.0f;
     }
     return v;
 }

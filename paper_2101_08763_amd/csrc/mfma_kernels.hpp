@@ -72,9 +72,12 @@ __global__ __launch_bounds__(64) void pack_tiles_kernel(const T *__restrict__ V,
     const bool valid = idx >= 0 && idx < n;
     unsigned char *tile = tiles + t * (int64_t)(HDR + nkb * 1024);
     typename M::vec_t *dst = reinterpret_cast<typename M::vec_t *>(tile + HDR);
+    const int64_t r = valid ? idx : n;  // row n reads as zeros
     float q = 0.0f;
     for (int kb = 0; kb < nkb; ++kb) {
-        const typename M::vec_t v = load_lanevec<M>(V, n, d, valid ? idx : n, kb, grp, vec_ok);
+        const typename M::vec_t v = vec_ok ? lanevec_keep<M>(lanevec_raw<M>(V, n, d, r, kb, grp),
+                                                             lanevec_live<M>(n, d, r, kb, grp))
+                                           : lanevec_scalar<M>(V, n, d, r, kb, grp);
         dst[kb * 64 + lane] = v;
 #pragma unroll
         for (int e = 0; e < M::VEC; ++e) {
@@ -93,7 +96,11 @@ __global__ __launch_bounds__(64) void pack_tiles_kernel(const T *__restrict__ V,
 // at least EXEMCL_STAGE_MIN bytes; large tiles go EXEMCL_TPS_BIG per stage.
 // A stage is rounded up to one 16-byte load per thread, at most two stages
 // share the 160 KiB of LDS, and the ring has up to EXEMCL_RING_SMALL /
-// EXEMCL_RING_BIG buffers.  Fewer, larger stages mean fewer barriers.
+// EXEMCL_RING_BIG buffers.  Fewer, larger stages mean fewer barriers.  Inside
+// a tile, up to EXEMCL_PF B fragments are read from LDS ahead of their use.
+#ifndef EXEMCL_PF
+#define EXEMCL_PF 3
+#endif
 #ifndef EXEMCL_SMALL_WAVES
 #define EXEMCL_SMALL_WAVES 4
 #endif
@@ -190,7 +197,7 @@ __global__ __launch_bounds__(WAVES * 64) void eval_mfma_kernel(const T *__restri
     constexpr int TPS = tiles_per_stage<NKB, WAVES>();
     constexpr int CNT = SB / (NT * 16);
     constexpr int NBUF = ring_depth<NKB, WAVES>();
-    constexpr int PF = NKB < 3 ? NKB : 3;  // B fragments in flight ahead of use
+    constexpr int PF = NKB < EXEMCL_PF ? NKB : EXEMCL_PF;  // B fragments in flight ahead of use
     static_assert(TPS >= 1 && TPS * TB <= SB && NBUF >= 2 && NBUF * SB <= kLdsBytes, "stage geometry");
     static_assert(CNT * (NBUF - 2) < 64, "vmcnt range");
     static_assert(NKS_LAST >= 1 && NKS_LAST <= M::KS_PER_KB, "k-steps of the last block");
@@ -235,10 +242,23 @@ __global__ __launch_bounds__(WAVES * 64) void eval_mfma_kernel(const T *__restri
     // Ground points of this wavefront, in A-operand order, resident for the
     // whole kernel (zero past d and past n).
     vec_t a[RT][NKB];
+    if (vec_ok) {
+        // All loads first (one batch in flight), then the zero selects.
 #pragma unroll
-    for (int rt = 0; rt < RT; ++rt)
+        for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
-        for (int kb = 0; kb < NKB; ++kb) a[rt][kb] = load_lanevec<M>(V, n, d, row0 + rt * TM + lr, kb, grp, vec_ok);
+            for (int kb = 0; kb < NKB; ++kb) a[rt][kb] = lanevec_raw<M>(V, n, d, row0 + rt * TM + lr, kb, grp);
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+            for (int kb = 0; kb < NKB; ++kb)
+                a[rt][kb] = lanevec_keep<M>(a[rt][kb], lanevec_live<M>(n, d, row0 + rt * TM + lr, kb, grp));
+    } else {
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+            for (int kb = 0; kb < NKB; ++kb) a[rt][kb] = lanevec_scalar<M>(V, n, d, row0 + rt * TM + lr, kb, grp);
+    }
 
     // Initial value of the running max for each output element: e0's 0, or
     // (HAS_M0) the per-point cached value when scoring S u {c}.
