@@ -111,25 +111,23 @@ __device__ __forceinline__ int out_row(int i, int grp) {
     return (i >> 2) * (4 * GROUPS) + 4 * grp + (i & 3);
 }
 
-// Lane vector of row `r` for k-block kb in MFMA operand order; coordinates
-// >= d and rows >= n read as zero.
-//
-// When rows are 16-byte aligned and hold whole lane vectors (`vec_ok`), a
-// vector is either entirely inside the row or entirely past d:
-// lanevec_raw loads it from a clamped, always in-bounds address and
-// lanevec_live says whether to keep it.  Callers issue every raw load of a
-// batch first and select afterwards, so the loads are in flight together.
+// Lane vector of row `r` for k-block kb in MFMA operand order, for rows of
+// `ld` elements that are whole 16-byte lane vectors (16-byte aligned, ld a
+// multiple of VEC, zero past the data's own d).  Rows >= n and vectors past
+// ld read as zero: lanevec_raw loads from a clamped, always in-bounds
+// address and lanevec_keep applies lanevec_live, so there is no divergent
+// branch.
 template <typename M, typename T>
-__device__ __forceinline__ typename M::vec_t lanevec_raw(const T *__restrict__ V, int64_t n, int d, int64_t r,
+__device__ __forceinline__ typename M::vec_t lanevec_raw(const T *__restrict__ V, int64_t n, int ld, int64_t r,
                                                          int kb, int grp) {
     const int d0 = M::dim(kb, grp, 0);
-    const bool live = r < n && d0 < d;
-    return *reinterpret_cast<const typename M::vec_t *>(V + (live ? r : 0) * (int64_t)d + (live ? d0 : 0));
+    const bool live = r < n && d0 < ld;
+    return *reinterpret_cast<const typename M::vec_t *>(V + (live ? r : 0) * (int64_t)ld + (live ? d0 : 0));
 }
 
 template <typename M>
-__device__ __forceinline__ bool lanevec_live(int64_t n, int d, int64_t r, int kb, int grp) {
-    return r < n && M::dim(kb, grp, 0) < d;
+__device__ __forceinline__ bool lanevec_live(int64_t n, int ld, int64_t r, int kb, int grp) {
+    return r < n && M::dim(kb, grp, 0) < ld;
 }
 
 template <typename M>
@@ -139,18 +137,22 @@ __device__ __forceinline__ typename M::vec_t lanevec_keep(typename M::vec_t v, b
     return z;
 }
 
-// Element-wise load for rows that are not whole aligned lane vectors.
-template <typename M, typename T>
-__device__ __forceinline__ typename M::vec_t lanevec_scalar(const T *__restrict__ V, int64_t n, int d, int64_t r,
-                                                            int kb, int grp) {
-    typename M::vec_t v;
-    const int d0 = M::dim(kb, grp, 0);
-    const T *row = V + (r < n ? r : 0) * (int64_t)d;
-    for (int e = 0; e < M::VEC; ++e) {
-        const int t = d0 + e;
-        v[e] = (r < n && t < d) ? row[t] : (T)0.0f;
-    }
-    return v;
+// Buffer resource over `bytes` bytes at `base`: raw buffer loads through it
+// return zero past the end instead of touching memory.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t window_rsrc(const void *base, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)bytes, 0x00020000);
+}
+
+// 16-byte load at byte offset `off` of a window; an offset at or past the
+// window's end (kDeadOffset) reads as zeros.
+constexpr uint32_t kDeadOffset = 0x80000000u;
+template <typename vec_t>
+__device__ __forceinline__ vec_t window_load16(__amdgpu_buffer_rsrc_t rsrc, uint32_t off) {
+    return __builtin_bit_cast(vec_t, __builtin_amdgcn_raw_buffer_load_b128(rsrc, (int)off, 0, 0));
+}
+
+__device__ __forceinline__ float window_load4(__amdgpu_buffer_rsrc_t rsrc, uint32_t off) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rsrc, (int)off, 0, 0));
 }
 
 }  // namespace exemcl

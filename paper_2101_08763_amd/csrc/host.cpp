@@ -164,6 +164,36 @@ int alloc_scratch(Scratch *s, int64_t bytes, hipStream_t st) {
 
 int status_of(hipError_t e) { return e == hipSuccess ? EXEMCL_OK : EXEMCL_EDEVICE; }
 
+int64_t elem_size(int precision) { return precision == EXEMCL_FP32 ? 4 : 2; }
+
+// V as the MFMA kernels read it: V itself when its rows are whole aligned
+// 16-byte lane vectors, else a zero-padded copy in temporary memory.
+struct MfmaRows {
+    const void *V = nullptr;
+    int64_t ld = 0;
+    int64_t bytes = 0;  // temporary memory held by the copy
+    Scratch copy;
+};
+
+int64_t pad_bytes(int precision, int64_t n, int64_t d) {
+    return (d * elem_size(precision)) % 16 == 0 ? 0 : align_up(n * mfma_row_stride(precision, d) * elem_size(precision), 256);
+}
+
+int prepare_rows(const void *V, int64_t n, int64_t d, int precision, hipStream_t st, MfmaRows *r) {
+    if (mfma_rows_ready(precision, V, d)) {
+        r->V = V;
+        r->ld = d;
+        return EXEMCL_OK;
+    }
+    r->ld = mfma_row_stride(precision, d);
+    r->bytes = align_up(n * r->ld * elem_size(precision), 256);
+    const int rc = alloc_scratch(&r->copy, r->bytes, st);
+    if (rc) return rc;
+    if (launch_pad(precision, V, n, (int)d, r->copy.ptr, (int)r->ld, st) != hipSuccess) return EXEMCL_EDEVICE;
+    r->V = r->copy.ptr;
+    return EXEMCL_OK;
+}
+
 // Event pairs around the dominant kernel, recorded while profiling is on.
 std::mutex g_prof_mu;
 bool g_prof_on = false;
@@ -200,18 +230,18 @@ struct ProfRange {
 };
 
 // Queue the evaluation of sets [0, l) with a workspace laid out by L.
-hipError_t run_chunk(const Layout &L, char *base, const void *V, int64_t n, int64_t d, const int32_t *sets,
-                     int64_t l, int64_t k, int precision, const float *m0, const int32_t *common, int64_t kcommon,
-                     float *out, hipStream_t st) {
+hipError_t run_chunk(const Layout &L, char *base, const void *V, int64_t n, int64_t d, const MfmaRows *rows,
+                     const int32_t *sets, int64_t l, int64_t k, int precision, const float *m0,
+                     const int32_t *common, int64_t kcommon, float *out, hipStream_t st) {
     if (L.path == EXEMCL_PATH_NONE) return launch_zero(out, l, st);  // k = 0: every set is empty
     float *partials = (float *)(base + L.off_partials);
     hipError_t e = hipSuccess;
     if (L.path == EXEMCL_PATH_MFMA) {
         void *tiles = base + L.off_tiles;
-        e = launch_pack(precision, L.mp, V, n, (int)d, sets, l, k, tiles, st);
+        e = launch_pack(precision, L.mp, rows->V, n, (int)rows->ld, sets, l, k, tiles, st);
         if (e == hipSuccess) {
             ProfRange pr(st);
-            e = launch_mfma(precision, MODE_SUM, L.mp, V, n, (int)d, tiles, k, L.ngroups, L.gpc, m0, partials,
+            e = launch_mfma(precision, MODE_SUM, L.mp, rows->V, n, (int)rows->ld, tiles, k, L.ngroups, L.gpc, m0, partials,
                             L.lpad, nullptr, st);
             pr.end();
         }
@@ -234,8 +264,13 @@ hipError_t run_chunk(const Layout &L, char *base, const void *V, int64_t n, int6
 // after another in one workspace.  A set's result does not depend on the
 // batch it is evaluated in, so chunked results are bitwise the same.  ENOMEM
 // only when not even one set group fits -- the paper's chunk size 0.
+//
+// `rows` (nullable) is V already prepared for the MFMA kernels by the caller,
+// which also holds `reserved` bytes of temporary memory that count against
+// EXEMCL_WORKSPACE_LIMIT.
 int run_eval(const void *V, int64_t n, int64_t d, const int32_t *sets, int64_t l, int64_t k, int precision,
-             const float *m0, const int32_t *common, int64_t kcommon, float *out, hipStream_t st) {
+             const float *m0, const int32_t *common, int64_t kcommon, float *out, hipStream_t st,
+             const MfmaRows *rows = nullptr, int64_t reserved = 0) {
     if (l == 0) return EXEMCL_OK;
     int path = k == 0 ? EXEMCL_PATH_NONE : choose_path(d, k, precision);
     if (m0 && path == EXEMCL_PATH_VALU) path = EXEMCL_PATH_MFMA;
@@ -243,7 +278,15 @@ int run_eval(const void *V, int64_t n, int64_t d, const int32_t *sets, int64_t l
     Layout L;
     if (!layout_eval(n, d, l, k, precision, path, &L)) return EXEMCL_EINVAL;
     const int64_t unit = path == EXEMCL_PATH_MFMA ? L.mp.tile : 1;
-    const int64_t limit = workspace_limit();
+    MfmaRows own;
+    if (path == EXEMCL_PATH_MFMA && !rows) {
+        if (reserved + pad_bytes(precision, n, d) > workspace_limit()) return EXEMCL_ENOMEM;
+        const int rc = prepare_rows(V, n, d, precision, st, &own);
+        if (rc) return rc;
+        rows = &own;
+        reserved += own.bytes;
+    }
+    const int64_t limit = workspace_limit() - reserved;
     int64_t lc = l;
     Scratch ws;
     for (;;) {
@@ -261,8 +304,8 @@ int run_eval(const void *V, int64_t n, int64_t d, const int32_t *sets, int64_t l
         const int64_t lj = l - j0 < lc ? l - j0 : lc;
         Layout Lj;
         if (!layout_eval(n, d, lj, k, precision, path, &Lj)) return EXEMCL_EINVAL;
-        const hipError_t e = run_chunk(Lj, base, V, n, d, sets + j0 * k, lj, k, precision, m0, common, kcommon,
-                                       out + j0, st);
+        const hipError_t e = run_chunk(Lj, base, V, n, d, rows, sets + j0 * k, lj, k, precision, m0, common,
+                                       kcommon, out + j0, st);
         if (e != hipSuccess) return EXEMCL_EDEVICE;
     }
     return EXEMCL_OK;
@@ -300,20 +343,24 @@ EXEMCL_API int exemplar_gain(const float *V, int64_t n, int64_t d, const int32_t
     const int64_t ngroups = (k + tm - 1) / tm;
     const int64_t off_tiles = align_up(n * 4, 256);
     const int64_t bytes = align_up(off_tiles + ngroups * tile_bytes(mp), 256);
+    if (bytes + pad_bytes(EXEMCL_FP32, n, d) > workspace_limit()) return EXEMCL_ENOMEM;
+    MfmaRows rows;
+    rc = prepare_rows(V, n, d, EXEMCL_FP32, st, &rows);
+    if (rc) return rc;
     Scratch ws;
     rc = alloc_scratch(&ws, bytes, st);
     if (rc) return rc;
     char *base = (char *)ws.ptr;
     float *gcache = (float *)base;
     void *tiles = base + off_tiles;
-    hipError_t e = launch_pack(EXEMCL_FP32, mp, V, n, (int)d, S, k, 1, tiles, st);
+    hipError_t e = launch_pack(EXEMCL_FP32, mp, rows.V, n, (int)rows.ld, S, k, 1, tiles, st);
     if (e == hipSuccess)
-        e = launch_mfma(EXEMCL_FP32, MODE_ROWMAX, mp, V, n, (int)d, tiles, 1, ngroups, ngroups, nullptr, nullptr, 0,
-                        gcache, st);
+        e = launch_mfma(EXEMCL_FP32, MODE_ROWMAX, mp, rows.V, n, (int)rows.ld, tiles, 1, ngroups, ngroups, nullptr,
+                        nullptr, 0, gcache, st);
     if (e != hipSuccess) return EXEMCL_EDEVICE;
     // Score every S u {c}: single-member sets {c} with the running max
     // started at g(v) instead of e0's 0.
-    return run_eval(V, n, d, cands, l, 1, EXEMCL_FP32, gcache, S, k, out, st);
+    return run_eval(V, n, d, cands, l, 1, EXEMCL_FP32, gcache, S, k, out, st, &rows, rows.bytes + bytes);
 }
 
 EXEMCL_API int exemplar_greedy(const float *V, int64_t n, int64_t d, int64_t K, int32_t *S_out, float *f_out,
@@ -343,7 +390,11 @@ EXEMCL_API int exemplar_greedy(const float *V, int64_t n, int64_t d, int64_t K, 
     // Candidates are scored in chunks whose temporary memory stays under a
     // fixed size (the same halving as for a batch that does not fit).
     constexpr int64_t kScoringBytes = int64_t(1) << 30;
-    const int64_t limit = workspace_limit();
+    const int64_t limit = workspace_limit() - pad_bytes(EXEMCL_FP32, n, d);
+    if (limit < fixed) return EXEMCL_ENOMEM;
+    MfmaRows rows;
+    int rc = prepare_rows(V, n, d, EXEMCL_FP32, st, &rows);
+    if (rc) return rc;
     int64_t lc = n;
     Layout L;
     Scratch ws;
@@ -351,7 +402,7 @@ EXEMCL_API int exemplar_greedy(const float *V, int64_t n, int64_t d, int64_t K, 
         if (!layout_eval(n, d, lc, 1, EXEMCL_FP32, EXEMCL_PATH_MFMA, &L)) return EXEMCL_EINVAL;
         const bool small = L.bytes <= kScoringBytes || lc <= mp.tile;
         if (small && fixed + L.bytes <= limit) {
-            const int rc = alloc_scratch(&ws, fixed + L.bytes, st);
+            rc = alloc_scratch(&ws, fixed + L.bytes, st);
             if (rc == EXEMCL_OK) break;
             if (rc != EXEMCL_ENOMEM) return rc;
         }
@@ -376,15 +427,16 @@ EXEMCL_API int exemplar_greedy(const float *V, int64_t n, int64_t d, int64_t K, 
             const int64_t lj = n - j0 < lc ? n - j0 : lc;
             Layout Lj;
             if (!layout_eval(n, d, lj, 1, EXEMCL_FP32, EXEMCL_PATH_MFMA, &Lj)) return EXEMCL_EINVAL;
-            e = run_chunk(Lj, work, V, n, d, cands + j0, lj, 1, EXEMCL_FP32, g_cur, nullptr, 0, scores + j0, st);
+            e = run_chunk(Lj, work, V, n, d, &rows, cands + j0, lj, 1, EXEMCL_FP32, g_cur, nullptr, 0, scores + j0,
+                          st);
         }
         if (e == hipSuccess) e = launch_argmax(scores, taken, n, pval, pidx, S_out + i, f_out + i, st);
         if (i + 1 == K) break;
         // g <- max(g, h_{c*}) with c* read from S_out[i] on the device.
-        if (e == hipSuccess) e = launch_pack(EXEMCL_FP32, mp, V, n, (int)d, S_out + i, 1, 1, ctile, st);
+        if (e == hipSuccess) e = launch_pack(EXEMCL_FP32, mp, rows.V, n, (int)rows.ld, S_out + i, 1, 1, ctile, st);
         if (e == hipSuccess)
-            e = launch_mfma(EXEMCL_FP32, MODE_ROWMAX, mp, V, n, (int)d, ctile, 1, 1, 1, g_cur, nullptr, 0, g_next,
-                            st);
+            e = launch_mfma(EXEMCL_FP32, MODE_ROWMAX, mp, rows.V, n, (int)rows.ld, ctile, 1, 1, 1, g_cur, nullptr, 0,
+                            g_next, st);
         std::swap(g_cur, g_next);
     }
     return status_of(e);
@@ -406,7 +458,7 @@ EXEMCL_API int exemplar_plan(int64_t n, int64_t d, int64_t l, int64_t k, int pre
     Layout L;
     if (!layout_eval(n, d, l, k, precision, p, &L)) return EXEMCL_EINVAL;
     if (path) *path = p;
-    if (workspace_bytes) *workspace_bytes = L.bytes;
+    if (workspace_bytes) *workspace_bytes = L.bytes + (p == EXEMCL_PATH_MFMA ? pad_bytes(precision, n, d) : 0);
     return EXEMCL_OK;
 }
 

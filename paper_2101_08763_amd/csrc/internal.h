@@ -31,7 +31,7 @@ bool mfma_plan(int prec, int64_t d, MfmaPlan *p);
 struct MfmaArgs {
     const void *V;
     int64_t n;
-    int d;
+    int ld;  // row stride in elements: rows are whole 16-byte lane vectors
     const void *tiles;
     int64_t k, ngroups, gpc;
     const float *m0;
@@ -41,11 +41,11 @@ struct MfmaArgs {
 };
 
 // Per-storage-type instantiations (kernels_mfma_{f32,f16,bf16}.hip).
-hipError_t pack_run_f32(const MfmaPlan &pl, const void *V, int64_t n, int d, const int32_t *sets, int64_t l,
+hipError_t pack_run_f32(const MfmaPlan &pl, const void *V, int64_t n, int ld, const int32_t *sets, int64_t l,
                         int64_t k, void *tiles, hipStream_t st);
-hipError_t pack_run_f16(const MfmaPlan &pl, const void *V, int64_t n, int d, const int32_t *sets, int64_t l,
+hipError_t pack_run_f16(const MfmaPlan &pl, const void *V, int64_t n, int ld, const int32_t *sets, int64_t l,
                         int64_t k, void *tiles, hipStream_t st);
-hipError_t pack_run_bf16(const MfmaPlan &pl, const void *V, int64_t n, int d, const int32_t *sets, int64_t l,
+hipError_t pack_run_bf16(const MfmaPlan &pl, const void *V, int64_t n, int ld, const int32_t *sets, int64_t l,
                          int64_t k, void *tiles, hipStream_t st);
 hipError_t eval_run_f32(const MfmaPlan &pl, int mode, const MfmaArgs &x, hipStream_t st);
 hipError_t eval_run_f16(const MfmaPlan &pl, int mode, const MfmaArgs &x, hipStream_t st);
@@ -62,10 +62,19 @@ struct ValuPlan {
 
 bool valu_plan(int prec, int64_t d, int64_t k, ValuPlan *p);
 
+// The MFMA kernels read V as rows of `ld` elements that are whole 16-byte
+// lane vectors: V 16-byte aligned, ld * element size a multiple of 16, zero
+// past the data's own d (mfma_row_stride, launch_pad).
+int64_t mfma_row_stride(int prec, int64_t d);
+bool mfma_rows_ready(int prec, const void *V, int64_t d);
+
+// Vp[i][t] = V[i][t] for t < d, 0 for d <= t < ld (n rows).
+hipError_t launch_pad(int prec, const void *V, int64_t n, int d, void *Vp, int ld, hipStream_t st);
+
 // Stage the exemplar tiles of `l` sets of `k` indices: for every (set group,
 // slot) pair one TM-column tile holding TM biases -||s||^2/2 (-FLT_MAX for
 // padding columns and invalid indices) and the B lane vectors.
-hipError_t launch_pack(int prec, const MfmaPlan &pl, const void *V, int64_t n, int d, const int32_t *sets,
+hipError_t launch_pack(int prec, const MfmaPlan &pl, const void *V, int64_t n, int ld, const int32_t *sets,
                        int64_t l, int64_t k, void *tiles, hipStream_t st);
 
 // Bytes of one staged tile (bias header + B lane vectors).
@@ -79,7 +88,7 @@ enum Mode { MODE_SUM = 0, MODE_ROWMAX = 1 };
 // when null (fp32 only otherwise).  MODE_ROWMAX (fp32, groups_per_chunk =
 // ngroups) instead writes rowmax[v] = max(m0(v), 0, max over all staged
 // columns); rowmax must not alias m0.
-hipError_t launch_mfma(int prec, int mode, const MfmaPlan &pl, const void *V, int64_t n, int d,
+hipError_t launch_mfma(int prec, int mode, const MfmaPlan &pl, const void *V, int64_t n, int ld,
                        const void *tiles, int64_t k, int64_t ngroups, int64_t groups_per_chunk,
                        const float *m0, float *partials, int64_t lpad, float *rowmax, hipStream_t st);
 

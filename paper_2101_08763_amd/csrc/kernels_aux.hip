@@ -225,6 +225,54 @@ hipError_t launch_reduce(const float *partials, int64_t G, int64_t lpad, int64_t
     return hipGetLastError();
 }
 
+// ---------------------------------------------------------------------------
+// Rows padded for the MFMA kernels: one thread per 16-byte output vector.
+// ---------------------------------------------------------------------------
+int64_t mfma_row_stride(int prec, int64_t d) {
+    const int64_t vec = prec == P_FP32 ? 4 : 8;
+    return (d + vec - 1) / vec * vec;
+}
+
+bool mfma_rows_ready(int prec, const void *V, int64_t d) {
+    const int64_t es = prec == P_FP32 ? 4 : 2;
+    return (uintptr_t)V % 16 == 0 && (d * es) % 16 == 0;
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void pad_rows_kernel(const T *__restrict__ V, int64_t n, int d, T *__restrict__ Vp,
+                                                       int ld) {
+    constexpr int VEC = 16 / sizeof(T);
+    const int64_t vpr = ld / VEC;
+    const int64_t q = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (q >= n * vpr) return;
+    const int64_t i = q / vpr;
+    const int t0 = (int)(q - i * vpr) * VEC;
+    T *dst = Vp + i * (int64_t)ld + t0;
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) dst[e] = t0 + e < d ? V[i * (int64_t)d + t0 + e] : (T)0.0f;
+}
+
+hipError_t launch_pad(int prec, const void *V, int64_t n, int d, void *Vp, int ld, hipStream_t st) {
+    const int64_t vec = prec == P_FP32 ? 4 : 8;
+    const int64_t blocks = (n * (ld / vec) + 255) / 256;
+    switch (prec) {
+    case P_FP32:
+        hipLaunchKernelGGL(pad_rows_kernel<float>, dim3((unsigned)blocks), dim3(256), 0, st, (const float *)V, n, d,
+                           (float *)Vp, ld);
+        break;
+    case P_FP16:
+        hipLaunchKernelGGL(pad_rows_kernel<_Float16>, dim3((unsigned)blocks), dim3(256), 0, st, (const _Float16 *)V, n,
+                           d, (_Float16 *)Vp, ld);
+        break;
+    case P_BF16:
+        hipLaunchKernelGGL(pad_rows_kernel<__bf16>, dim3((unsigned)blocks), dim3(256), 0, st, (const __bf16 *)V, n, d,
+                           (__bf16 *)Vp, ld);
+        break;
+    default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
 // f of empty sets (k = 0): out[j] = 0, e0 alone.
 __global__ __launch_bounds__(256) void zero_kernel(float *__restrict__ out, int64_t count) {
     const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;

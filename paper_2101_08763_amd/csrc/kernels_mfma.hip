@@ -52,20 +52,20 @@ bool mfma_plan(int prec, int64_t d, MfmaPlan *p) {
 
 int64_t mfma_tile_bytes(const MfmaPlan &pl) { return HDR + (int64_t)pl.nkb * 1024; }
 
-hipError_t launch_pack(int prec, const MfmaPlan &pl, const void *V, int64_t n, int d, const int32_t *sets,
+hipError_t launch_pack(int prec, const MfmaPlan &pl, const void *V, int64_t n, int ld, const int32_t *sets,
                        int64_t l, int64_t k, void *tiles, hipStream_t st) {
     switch (prec) {
-    case P_FP32: return pack_run_f32(pl, V, n, d, sets, l, k, tiles, st);
-    case P_FP16: return pack_run_f16(pl, V, n, d, sets, l, k, tiles, st);
-    case P_BF16: return pack_run_bf16(pl, V, n, d, sets, l, k, tiles, st);
+    case P_FP32: return pack_run_f32(pl, V, n, ld, sets, l, k, tiles, st);
+    case P_FP16: return pack_run_f16(pl, V, n, ld, sets, l, k, tiles, st);
+    case P_BF16: return pack_run_bf16(pl, V, n, ld, sets, l, k, tiles, st);
     }
     return hipErrorInvalidValue;
 }
 
-hipError_t launch_mfma(int prec, int mode, const MfmaPlan &pl, const void *V, int64_t n, int d, const void *tiles,
+hipError_t launch_mfma(int prec, int mode, const MfmaPlan &pl, const void *V, int64_t n, int ld, const void *tiles,
                        int64_t k, int64_t ngroups, int64_t gpc, const float *m0, float *partials, int64_t lpad,
                        float *rowmax, hipStream_t st) {
-    const MfmaArgs x{V, n, d, tiles, k, ngroups, gpc, m0, partials, lpad, rowmax};
+    const MfmaArgs x{V, n, ld, tiles, k, ngroups, gpc, m0, partials, lpad, rowmax};
     switch (prec) {
     case P_FP32: return eval_run_f32(pl, mode, x, st);
     case P_FP16: return mode == MODE_SUM ? eval_run_f16(pl, mode, x, st) : hipErrorInvalidValue;

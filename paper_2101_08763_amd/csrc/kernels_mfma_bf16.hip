@@ -4,9 +4,9 @@
 
 namespace exemcl {
 
-hipError_t pack_run_bf16(const MfmaPlan &pl, const void *V, int64_t n, int d, const int32_t *sets, int64_t l,
+hipError_t pack_run_bf16(const MfmaPlan &pl, const void *V, int64_t n, int ld, const int32_t *sets, int64_t l,
                          int64_t k, void *tiles, hipStream_t st) {
-    return pack_launch<__bf16, 32>(pl, V, n, d, sets, l, k, tiles, st);
+    return pack_launch<__bf16, 32>(pl, V, n, ld, sets, l, k, tiles, st);
 }
 
 hipError_t eval_run_bf16(const MfmaPlan &pl, int mode, const MfmaArgs &x, hipStream_t st) {

@@ -52,15 +52,15 @@ constexpr int tile_bytes_of() {
 //   [HDR + kb*1024 + 16*L)  lane L's 16-byte B-operand vector for k-block kb
 // Padding columns (set >= l), empty slots and invalid indices become zero
 // vectors with bias -FLT_MAX, which never wins the running max.
-// Coordinates past d are zero.  One wavefront per tile; ||s||^2 is summed
+// Rows are ld elements, zero past the data's d.  One wavefront per tile;
+// ||s||^2 is summed
 // from the lane vectors (fp32, k-blocks then elements in order, then the
 // K-groups of the column with a fixed xor tree).
 // ---------------------------------------------------------------------------
 template <typename T, int TILE>
-__global__ __launch_bounds__(64) void pack_tiles_kernel(const T *__restrict__ V, int64_t n, int d,
+__global__ __launch_bounds__(64) void pack_tiles_kernel(const T *__restrict__ V, int64_t n, int ld,
                                                         const int32_t *__restrict__ sets, int64_t l,
-                                                        int64_t k, int nkb, unsigned char *__restrict__ tiles,
-                                                        bool vec_ok) {
+                                                        int64_t k, int nkb, unsigned char *__restrict__ tiles) {
     using M = Mfma<T, TILE>;
     const int64_t t = blockIdx.x;
     const int64_t g = t / k, p = t - (t / k) * k;
@@ -75,9 +75,8 @@ __global__ __launch_bounds__(64) void pack_tiles_kernel(const T *__restrict__ V,
     const int64_t r = valid ? idx : n;  // row n reads as zeros
     float q = 0.0f;
     for (int kb = 0; kb < nkb; ++kb) {
-        const typename M::vec_t v = vec_ok ? lanevec_keep<M>(lanevec_raw<M>(V, n, d, r, kb, grp),
-                                                             lanevec_live<M>(n, d, r, kb, grp))
-                                           : lanevec_scalar<M>(V, n, d, r, kb, grp);
+        const typename M::vec_t v =
+            lanevec_keep<M>(lanevec_raw<M>(V, n, ld, r, kb, grp), lanevec_live<M>(n, ld, r, kb, grp));
         dst[kb * 64 + lane] = v;
 #pragma unroll
         for (int e = 0; e < M::VEC; ++e) {
@@ -100,6 +99,15 @@ __global__ __launch_bounds__(64) void pack_tiles_kernel(const T *__restrict__ V,
 // a tile, up to EXEMCL_PF B fragments are read from LDS ahead of their use.
 #ifndef EXEMCL_PF
 #define EXEMCL_PF 3
+#endif
+#ifndef EXEMCL_PAIR
+#define EXEMCL_PAIR 1
+#endif
+#ifndef EXEMCL_PAIR_NKB32
+#define EXEMCL_PAIR_NKB32 8
+#endif
+#ifndef EXEMCL_PAIR_NKB16
+#define EXEMCL_PAIR_NKB16 4
 #endif
 #ifndef EXEMCL_SMALL_WAVES
 #define EXEMCL_SMALL_WAVES 4
@@ -181,12 +189,12 @@ __device__ __forceinline__ void wait_vmcnt() {
 // h_s(v)) (m0 = 0 when null); rowmax must not alias m0.
 // ---------------------------------------------------------------------------
 template <typename T, int TILE, int NKB, int NKS_LAST, int RT, int WAVES, int MODE, bool HAS_M0>
-__global__ __launch_bounds__(WAVES * 64) void eval_mfma_kernel(const T *__restrict__ V, int64_t n, int d,
+__global__ __launch_bounds__(WAVES * 64) void eval_mfma_kernel(const T *__restrict__ V, int64_t n, int ld,
                                                                  const unsigned char *__restrict__ tiles, int64_t k,
                                                                  int64_t ngroups, int64_t gpc,
                                                                  const float *__restrict__ m0,
                                                                  float *__restrict__ partials, int64_t lpad,
-                                                                 float *__restrict__ rowmax, bool vec_ok) {
+                                                                 float *__restrict__ rowmax) {
     using M = Mfma<T, TILE>;
     using vec_t = typename M::vec_t;
     using acc_t = typename M::acc_t;
@@ -198,6 +206,7 @@ __global__ __launch_bounds__(WAVES * 64) void eval_mfma_kernel(const T *__restri
     constexpr int CNT = SB / (NT * 16);
     constexpr int NBUF = ring_depth<NKB, WAVES>();
     constexpr int PF = NKB < EXEMCL_PF ? NKB : EXEMCL_PF;  // B fragments in flight ahead of use
+    constexpr bool PAIR = EXEMCL_PAIR && NKB <= (sizeof(T) == 4 ? EXEMCL_PAIR_NKB32 : EXEMCL_PAIR_NKB16);
     static_assert(TPS >= 1 && TPS * TB <= SB && NBUF >= 2 && NBUF * SB <= kLdsBytes, "stage geometry");
     static_assert(CNT * (NBUF - 2) < 64, "vmcnt range");
     static_assert(NKS_LAST >= 1 && NKS_LAST <= M::KS_PER_KB, "k-steps of the last block");
@@ -242,35 +251,31 @@ __global__ __launch_bounds__(WAVES * 64) void eval_mfma_kernel(const T *__restri
     // Ground points of this wavefront, in A-operand order, resident for the
     // whole kernel (zero past d and past n).
     vec_t a[RT][NKB];
-    if (vec_ok) {
-        // All loads first (one batch in flight), then the zero selects.
+    // The workgroup's rows as one buffer window (at most 512 rows of at most
+    // 512 elements, so 32-bit offsets): rows past n read as zeros, and so do
+    // vectors past ld, without a branch.
+    const int64_t wrow0 = rb * (int64_t)(WAVES * RT * TM);
+    const int64_t wrows = min((int64_t)(WAVES * RT * TM), n - wrow0);
+    const auto vwin = window_rsrc(V + wrow0 * (int64_t)ld, (uint32_t)(wrows * ld * (int64_t)sizeof(T)));
 #pragma unroll
-        for (int rt = 0; rt < RT; ++rt)
+    for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
-            for (int kb = 0; kb < NKB; ++kb) a[rt][kb] = lanevec_raw<M>(V, n, d, row0 + rt * TM + lr, kb, grp);
-#pragma unroll
-        for (int rt = 0; rt < RT; ++rt)
-#pragma unroll
-            for (int kb = 0; kb < NKB; ++kb)
-                a[rt][kb] = lanevec_keep<M>(a[rt][kb], lanevec_live<M>(n, d, row0 + rt * TM + lr, kb, grp));
-    } else {
-#pragma unroll
-        for (int rt = 0; rt < RT; ++rt)
-#pragma unroll
-            for (int kb = 0; kb < NKB; ++kb) a[rt][kb] = lanevec_scalar<M>(V, n, d, row0 + rt * TM + lr, kb, grp);
-    }
+        for (int kb = 0; kb < NKB; ++kb) {
+            const int d0 = M::dim(kb, grp, 0);
+            const int lrow = wave * RT * TM + rt * TM + lr;
+            a[rt][kb] = window_load16<vec_t>(vwin, d0 < ld ? (uint32_t)((lrow * ld + d0) * (int)sizeof(T)) : kDeadOffset);
+        }
 
     // Initial value of the running max for each output element: e0's 0, or
     // (HAS_M0) the per-point cached value when scoring S u {c}.
     float minit[HAS_M0 ? RT : 1][HAS_M0 ? M::ACC : 1];
     if constexpr (HAS_M0) {
+        const auto mwin = window_rsrc(m0 + wrow0, (uint32_t)(wrows * 4));
 #pragma unroll
         for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
-            for (int i = 0; i < M::ACC; ++i) {
-                const int64_t r = row0 + rt * TM + out_row<TM>(i, grp);
-                minit[rt][i] = r < n ? m0[r] : 0.0f;
-            }
+            for (int i = 0; i < M::ACC; ++i)
+                minit[rt][i] = window_load4(mwin, (uint32_t)((wave * RT * TM + rt * TM + out_row<TM>(i, grp)) * 4));
     }
     auto m_init = [&](int rt, int i) -> float {
         if constexpr (HAS_M0) return minit[rt][i];
@@ -281,6 +286,33 @@ __global__ __launch_bounds__(WAVES * 64) void eval_mfma_kernel(const T *__restri
     for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
         for (int i = 0; i < M::ACC; ++i) m[rt][i] = m_init(rt, i);
+
+    // One tile: the bias enters as the accumulators' initial value (fp32),
+    // then the branch-free MFMA chain over the NKB k-blocks, B fragments read
+    // from LDS up to PF ahead of use.
+    auto chain = [&](const unsigned char *tb, acc_t (&acc)[RT]) {
+        const vec_t *B = reinterpret_cast<const vec_t *>(tb + HDR);
+        vec_t bq[PF];
+#pragma unroll
+        for (int i = 0; i < PF; ++i) bq[i] = B[i * 64 + lane];
+        const float b = reinterpret_cast<const float *>(tb)[lr];
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+            for (int i = 0; i < M::ACC; ++i) acc[rt][i] = b;
+#pragma unroll
+        for (int kb = 0; kb < NKB; ++kb) {
+            const vec_t bv = bq[kb % PF];
+            if (kb + PF < NKB) bq[kb % PF] = B[(kb + PF) * 64 + lane];
+#pragma unroll
+            for (int e = 0; e < M::KS_PER_KB; ++e) {
+                if (kb < NKB - 1 || e < NKS_LAST) {
+#pragma unroll
+                    for (int rt = 0; rt < RT; ++rt) acc[rt] = M::mma(a[rt][kb], bv, e, acc[rt]);
+                }
+            }
+        }
+    };
 
     float *wpart = partials + (rb * WAVES + wave) * lpad;
     int64_t g = g0;
@@ -293,58 +325,68 @@ __global__ __launch_bounds__(WAVES * 64) void eval_mfma_kernel(const T *__restri
 
         const unsigned char *buf = smem + (int)(s % NBUF) * SB;
         const int tn = (int)min((int64_t)TPS, ntiles - s * TPS);
-        for (int tt = 0; tt < tn; ++tt) {
-            const unsigned char *tb = buf + tt * TB;
-            const vec_t *B = reinterpret_cast<const vec_t *>(tb + HDR);
-            vec_t bq[PF];
-#pragma unroll
-            for (int i = 0; i < PF; ++i) bq[i] = B[i * 64 + lane];
-            const float b = reinterpret_cast<const float *>(tb)[lr];
-
-            // The bias enters as the accumulator's initial value, in fp32.
-            acc_t acc[RT];
-#pragma unroll
-            for (int rt = 0; rt < RT; ++rt)
-#pragma unroll
-                for (int i = 0; i < M::ACC; ++i) acc[rt][i] = b;
-#pragma unroll
-            for (int kb = 0; kb < NKB; ++kb) {
-                const vec_t bv = bq[kb % PF];
-                if (kb + PF < NKB) bq[kb % PF] = B[(kb + PF) * 64 + lane];
-#pragma unroll
-                for (int e = 0; e < M::KS_PER_KB; ++e) {
-                    if (kb < NKB - 1 || e < NKS_LAST) {
-#pragma unroll
-                        for (int rt = 0; rt < RT; ++rt) acc[rt] = M::mma(a[rt][kb], bv, e, acc[rt]);
-                    }
-                }
-            }
-#pragma unroll
-            for (int rt = 0; rt < RT; ++rt)
-#pragma unroll
-                for (int i = 0; i < M::ACC; ++i) m[rt][i] = fmaxf(m[rt][i], acc[rt][i]);
-
+        // Close set group g after its last member: sum this lane's rows for
+        // its column, then the K-groups holding the other rows of the same
+        // column, and restart the running max.
+        auto group_end = [&]() {
             if constexpr (MODE == MODE_SUM) {
-                if (p == k - 1) {
-                    // Sum this lane's rows for its column, then the K-groups
-                    // holding the other rows of the same column.
-                    float sum = 0.0f;
+                float sum = 0.0f;
+#pragma unroll
+                for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+                    for (int i = 0; i < M::ACC; ++i) sum += m[rt][i];
+#pragma unroll
+                for (int off = TM; off < 64; off <<= 1) sum += __shfl_xor(sum, off);
+                if (grp == 0) wpart[g * TM + lr] = sum;
+#pragma unroll
+                for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+                    for (int i = 0; i < M::ACC; ++i) m[rt][i] = m_init(rt, i);
+            }
+        };
+        if constexpr (PAIR) {
+            int tt = 0;
+            while (tt < tn) {
+                if (tt + 1 < tn && p + 1 < k) {
+                    // Two members of the same set group: one max3 per element.
+                    acc_t x[RT], y[RT];
+                    chain(buf + tt * TB, x);
+                    chain(buf + (tt + 1) * TB, y);
 #pragma unroll
                     for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
-                        for (int i = 0; i < M::ACC; ++i) sum += m[rt][i];
-#pragma unroll
-                    for (int off = TM; off < 64; off <<= 1) sum += __shfl_xor(sum, off);
-                    if (grp == 0) wpart[g * TM + lr] = sum;
+                        for (int i = 0; i < M::ACC; ++i) m[rt][i] = fmaxf(fmaxf(m[rt][i], x[rt][i]), y[rt][i]);
+                    tt += 2;
+                    p += 2;
+                } else {
+                    acc_t x[RT];
+                    chain(buf + tt * TB, x);
 #pragma unroll
                     for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
-                        for (int i = 0; i < M::ACC; ++i) m[rt][i] = m_init(rt, i);
+                        for (int i = 0; i < M::ACC; ++i) m[rt][i] = fmaxf(m[rt][i], x[rt][i]);
+                    tt += 1;
+                    p += 1;
+                }
+                if (p == k) {
+                    group_end();
+                    p = 0;
+                    ++g;
                 }
             }
-            if (++p == k) {
-                p = 0;
-                ++g;
+        } else {
+            for (int tt = 0; tt < tn; ++tt) {
+                acc_t x[RT];
+                chain(buf + tt * TB, x);
+#pragma unroll
+                for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+                    for (int i = 0; i < M::ACC; ++i) m[rt][i] = fmaxf(m[rt][i], x[rt][i]);
+                if (p == k - 1) group_end();
+                if (++p == k) {
+                    p = 0;
+                    ++g;
+                }
             }
         }
     }
@@ -377,12 +419,11 @@ __global__ __launch_bounds__(WAVES * 64) void eval_mfma_kernel(const T *__restri
 // Host-side launch helpers.
 // ---------------------------------------------------------------------------
 template <typename T, int TILE>
-hipError_t pack_launch(const MfmaPlan &pl, const void *V, int64_t n, int d, const int32_t *sets, int64_t l,
+hipError_t pack_launch(const MfmaPlan &pl, const void *V, int64_t n, int ld, const int32_t *sets, int64_t l,
                        int64_t k, void *tiles, hipStream_t st) {
     const int64_t ngroups = (l + TILE - 1) / TILE;
-    const bool vec_ok = ((uintptr_t)V % 16 == 0) && ((d * (int64_t)sizeof(T)) % 16 == 0);
     hipLaunchKernelGGL((pack_tiles_kernel<T, TILE>), dim3((unsigned)(ngroups * k)), dim3(64), 0, st,
-                       (const T *)V, n, d, sets, l, k, pl.nkb, (unsigned char *)tiles, vec_ok);
+                       (const T *)V, n, ld, sets, l, k, pl.nkb, (unsigned char *)tiles);
     return hipGetLastError();
 }
 
@@ -399,10 +440,9 @@ hipError_t eval_launch_t(const MfmaArgs &x, hipStream_t st) {
     const int64_t rows = (int64_t)WAVES * RT * TILE;
     const int64_t G = (x.n + rows - 1) / rows;
     const int64_t chunks = (x.ngroups + x.gpc - 1) / x.gpc;
-    const bool vec_ok = ((uintptr_t)x.V % 16 == 0) && ((x.d * (int64_t)sizeof(T)) % 16 == 0);
     hipLaunchKernelGGL(kern, dim3((unsigned)G, (unsigned)chunks), dim3(WAVES * 64), lds, st, (const T *)x.V, x.n,
-                       x.d, (const unsigned char *)x.tiles, x.k, x.ngroups, x.gpc, x.m0, x.partials, x.lpad,
-                       x.rowmax, vec_ok);
+                       x.ld, (const unsigned char *)x.tiles, x.k, x.ngroups, x.gpc, x.m0, x.partials, x.lpad,
+                       x.rowmax);
     return hipGetLastError();
 }
 
