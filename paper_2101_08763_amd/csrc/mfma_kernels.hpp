@@ -226,20 +226,17 @@ __global__ __launch_bounds__(WAVES * 64) void eval_mfma_kernel(const T *__restri
     const unsigned char *chunk = tiles + g0 * k * (int64_t)TB;
     const int64_t chunk_bytes = ntiles * (int64_t)TB;
 
-    // Queue the direct-to-LDS copy of stage s (CNT loads per thread; loads past
-    // the chunk end re-read its first bytes into unused buffer space).
+    // Queue the direct-to-LDS copy of stage s (CNT 16-byte loads per thread).
     auto issue = [&](int64_t s) {
         unsigned char *buf = smem + (int)(s % NBUF) * SB;
         const int64_t base = s * (int64_t)(TPS * TB);
-        const int64_t end = min(chunk_bytes, base + (int64_t)(TPS * TB));
+        // A window over this stage's bytes: loads past the chunk end read zeros.
+        const auto win = window_rsrc(chunk + base, (uint32_t)min((int64_t)(TPS * TB), chunk_bytes - base));
 #pragma unroll
-        for (int r = 0; r < CNT; ++r) {
-            const int64_t off = base + (int64_t)(r * NT + tid) * 16;
-            const unsigned char *src = off < end ? chunk + off : chunk;
-            __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void *)src,
-                                             (__attribute__((address_space(3))) void *)(buf + (r * NT + wave * 64) * 16),
-                                             16, 0, 0);
-        }
+        for (int r = 0; r < CNT; ++r)
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                win, (__attribute__((address_space(3))) void *)(buf + (r * NT + wave * 64) * 16), 16,
+                (r * NT + tid) * 16, 0, 0, 0);
     };
 
     if (nstages > 0) {
