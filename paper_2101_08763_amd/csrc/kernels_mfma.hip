@@ -27,7 +27,7 @@ bool mfma_plan(int prec, int64_t d, MfmaPlan *p) {
         q.kb_dims = 8;
         q.nkb = bucket((int)((d + 7) / 8));
         q.nks_last = q.nkb == 1 ? (int)(d < 4 ? d : 4) : 4;  // instruction e covers dims e and 4 + e
-        q.rt = q.nkb <= 16 ? 2 : 1;
+        q.rt = q.nkb <= EXEMCL_RT1_NKB32 ? 1 : q.nkb <= 16 ? 2 : 1;  // as rt_small<float, NKB>()
     } else if (prec == P_FP32) {
         // v_mfma_f32_16x16x4_f32, 16 coordinates per k-block
         q.tile = 16;

@@ -103,6 +103,9 @@ __global__ __launch_bounds__(64) void pack_tiles_kernel(const T *__restrict__ V,
 #ifndef EXEMCL_PAIR
 #define EXEMCL_PAIR 1
 #endif
+#ifndef EXEMCL_RT1_NKB32
+#define EXEMCL_RT1_NKB32 0
+#endif
 #ifndef EXEMCL_PAIR_NKB32
 #define EXEMCL_PAIR_NKB32 8
 #endif
@@ -457,6 +460,13 @@ constexpr int waves_for() {
     return NKB <= EXEMCL_BIG_NKB ? EXEMCL_SMALL_WAVES : EXEMCL_BIG_WAVES;
 }
 
+// Row tiles per wavefront for buckets up to 16 k-blocks: 2, except fp32
+// buckets up to EXEMCL_RT1_NKB32 k-blocks (the plan uses the same rule).
+template <typename T, int NKB>
+constexpr int rt_small() {
+    return (sizeof(T) == 4 && NKB <= EXEMCL_RT1_NKB32) ? 1 : 2;
+}
+
 // One storage type: pick the instantiation for the plan's k-block bucket.
 template <typename T, int TILE, int MODE>
 hipError_t eval_dispatch(const MfmaPlan &pl, const MfmaArgs &x, hipStream_t st) {
@@ -472,29 +482,29 @@ hipError_t eval_dispatch(const MfmaPlan &pl, const MfmaArgs &x, hipStream_t st) 
         if (pl.nkb == 1) {
             if constexpr (KL == 4) {
                 switch (pl.nks_last) {
-                case 1: return eval_launch<T, TILE, 1, 1, 2, waves_for<1>(), MODE>(x, st);
-                case 2: return eval_launch<T, TILE, 1, 2, 2, waves_for<1>(), MODE>(x, st);
-                case 3: return eval_launch<T, TILE, 1, 3, 2, waves_for<1>(), MODE>(x, st);
-                case 4: return eval_launch<T, TILE, 1, 4, 2, waves_for<1>(), MODE>(x, st);
+                case 1: return eval_launch<T, TILE, 1, 1, rt_small<T, 1>(), waves_for<1>(), MODE>(x, st);
+                case 2: return eval_launch<T, TILE, 1, 2, rt_small<T, 1>(), waves_for<1>(), MODE>(x, st);
+                case 3: return eval_launch<T, TILE, 1, 3, rt_small<T, 1>(), waves_for<1>(), MODE>(x, st);
+                case 4: return eval_launch<T, TILE, 1, 4, rt_small<T, 1>(), waves_for<1>(), MODE>(x, st);
                 }
                 return hipErrorInvalidValue;
             } else {
-                return eval_launch<T, TILE, 1, KL, 2, waves_for<1>(), MODE>(x, st);
+                return eval_launch<T, TILE, 1, KL, rt_small<T, 1>(), waves_for<1>(), MODE>(x, st);
             }
         }
         switch (pl.nkb) {
-        case 2: return eval_launch<T, TILE, 2, KL, 2, waves_for<2>(), MODE>(x, st);
-        case 3: return eval_launch<T, TILE, 3, KL, 2, waves_for<3>(), MODE>(x, st);
-        case 4: return eval_launch<T, TILE, 4, KL, 2, waves_for<4>(), MODE>(x, st);
-        case 5: return eval_launch<T, TILE, 5, KL, 2, waves_for<5>(), MODE>(x, st);
-        case 6: return eval_launch<T, TILE, 6, KL, 2, waves_for<6>(), MODE>(x, st);
-        case 7: return eval_launch<T, TILE, 7, KL, 2, waves_for<7>(), MODE>(x, st);
-        case 8: return eval_launch<T, TILE, 8, KL, 2, waves_for<8>(), MODE>(x, st);
-        case 10: return eval_launch<T, TILE, 10, KL, 2, waves_for<10>(), MODE>(x, st);
-        case 12: return eval_launch<T, TILE, 12, KL, 2, waves_for<12>(), MODE>(x, st);
-        case 13: return eval_launch<T, TILE, 13, KL, 2, waves_for<13>(), MODE>(x, st);
-        case 14: return eval_launch<T, TILE, 14, KL, 2, waves_for<14>(), MODE>(x, st);
-        case 16: return eval_launch<T, TILE, 16, KL, 2, waves_for<16>(), MODE>(x, st);
+        case 2: return eval_launch<T, TILE, 2, KL, rt_small<T, 2>(), waves_for<2>(), MODE>(x, st);
+        case 3: return eval_launch<T, TILE, 3, KL, rt_small<T, 3>(), waves_for<3>(), MODE>(x, st);
+        case 4: return eval_launch<T, TILE, 4, KL, rt_small<T, 4>(), waves_for<4>(), MODE>(x, st);
+        case 5: return eval_launch<T, TILE, 5, KL, rt_small<T, 5>(), waves_for<5>(), MODE>(x, st);
+        case 6: return eval_launch<T, TILE, 6, KL, rt_small<T, 6>(), waves_for<6>(), MODE>(x, st);
+        case 7: return eval_launch<T, TILE, 7, KL, rt_small<T, 7>(), waves_for<7>(), MODE>(x, st);
+        case 8: return eval_launch<T, TILE, 8, KL, rt_small<T, 8>(), waves_for<8>(), MODE>(x, st);
+        case 10: return eval_launch<T, TILE, 10, KL, rt_small<T, 10>(), waves_for<10>(), MODE>(x, st);
+        case 12: return eval_launch<T, TILE, 12, KL, rt_small<T, 12>(), waves_for<12>(), MODE>(x, st);
+        case 13: return eval_launch<T, TILE, 13, KL, rt_small<T, 13>(), waves_for<13>(), MODE>(x, st);
+        case 14: return eval_launch<T, TILE, 14, KL, rt_small<T, 14>(), waves_for<14>(), MODE>(x, st);
+        case 16: return eval_launch<T, TILE, 16, KL, rt_small<T, 16>(), waves_for<16>(), MODE>(x, st);
         case 20: return eval_launch<T, TILE, 20, KL, 1, waves_for<20>(), MODE>(x, st);
         case 24: return eval_launch<T, TILE, 24, KL, 1, waves_for<24>(), MODE>(x, st);
         case 28: return eval_launch<T, TILE, 28, KL, 1, waves_for<28>(), MODE>(x, st);
