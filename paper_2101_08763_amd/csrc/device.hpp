@@ -23,6 +23,11 @@ __device__ __forceinline__ float to_f32(float x) { return x; }
 __device__ __forceinline__ float to_f32(_Float16 x) { return (float)x; }
 __device__ __forceinline__ float to_f32(__bf16 x) { return (float)x; }
 
+// Set members per staged tile for the 16x16x32 shape (see Mfma<_Float16, 16>).
+#ifndef EXEMCL_NB16
+#define EXEMCL_NB16 2
+#endif
+
 // One MFMA shape, seen from one lane.
 //
 //   TM      output tile is TM x TM (rows = ground points, columns = exemplars)
@@ -32,6 +37,9 @@ __device__ __forceinline__ float to_f32(__bf16 x) { return (float)x; }
 //   KS_PER_KB  instructions fed by one 16-byte lane vector (a "k-block")
 //   KB_DIMS    coordinates covered by one k-block across the wavefront
 //   ACC     fp32 accumulators per lane
+//   NB      set members per staged tile: NB groups of TM exemplar columns
+//           (member q*NB + h of the same TM sets in column group h), so the
+//           minimum over a set's members is also taken across the groups
 //
 // Coordinate of lane-vector element e, for a lane in K-group `grp`, inside
 // k-block kb: dim(kb, grp, e) = kb*KB_DIMS + grp*VEC + e, so every lane
@@ -47,7 +55,7 @@ struct Mfma;
 template <>
 struct Mfma<float, 32> {
     static constexpr int TM = 32, GROUPS = 2, VEC = 4;
-    static constexpr int KS_PER_KB = 4, KB_DIMS = 8, ACC = 16;
+    static constexpr int KS_PER_KB = 4, KB_DIMS = 8, ACC = 16, NB = 1;
     using acc_t = f32x16;
     using vec_t = f32x4;
     using elem_t = float;
@@ -63,7 +71,7 @@ struct Mfma<float, 32> {
 template <>
 struct Mfma<float, 16> {
     static constexpr int TM = 16, GROUPS = 4, VEC = 4;
-    static constexpr int KS_PER_KB = 4, KB_DIMS = 16, ACC = 4;
+    static constexpr int KS_PER_KB = 4, KB_DIMS = 16, ACC = 4, NB = 1;
     using acc_t = f32x4;
     using vec_t = f32x4;
     using elem_t = float;
@@ -78,7 +86,7 @@ struct Mfma<float, 16> {
 template <>
 struct Mfma<_Float16, 32> {
     static constexpr int TM = 32, GROUPS = 2, VEC = 8;
-    static constexpr int KS_PER_KB = 1, KB_DIMS = 16, ACC = 16;
+    static constexpr int KS_PER_KB = 1, KB_DIMS = 16, ACC = 16, NB = 1;
     using acc_t = f32x16;
     using vec_t = f16x8;
     using elem_t = _Float16;
@@ -92,13 +100,48 @@ struct Mfma<_Float16, 32> {
 template <>
 struct Mfma<__bf16, 32> {
     static constexpr int TM = 32, GROUPS = 2, VEC = 8;
-    static constexpr int KS_PER_KB = 1, KB_DIMS = 16, ACC = 16;
+    static constexpr int KS_PER_KB = 1, KB_DIMS = 16, ACC = 16, NB = 1;
     using acc_t = f32x16;
     using vec_t = bf16x8;
     using elem_t = __bf16;
     __device__ __forceinline__ static int dim(int kb, int grp, int e) { return kb * KB_DIMS + grp * VEC + e; }
     __device__ __forceinline__ static acc_t mma(vec_t a, vec_t b, int, acc_t c) {
         return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+    }
+};
+
+// fp16: v_mfma_f32_16x16x32_f16 (gfx950), 16 rows per tile, 32 coordinates
+// per instruction: lane L holds row / column L % 16 and coordinates
+// kb*32 + (L/16)*8 + {0..7}.  On random data this shape sustains a markedly
+// higher rate than the 32x32x16 one (the matrix cores draw less power per
+// flop, so the clock stays higher), so it serves every d above one 16-wide
+// k-block.  A staged tile holds two members of 16 sets (NB = 2): each A
+// fragment feeds two instructions, and a tile carries twice the work of a
+// single-member one for the same per-tile bookkeeping.
+template <>
+struct Mfma<_Float16, 16> {
+    static constexpr int TM = 16, GROUPS = 4, VEC = 8;
+    static constexpr int KS_PER_KB = 1, KB_DIMS = 32, ACC = 4, NB = EXEMCL_NB16;
+    using acc_t = f32x4;
+    using vec_t = f16x8;
+    using elem_t = _Float16;
+    __device__ __forceinline__ static int dim(int kb, int grp, int e) { return kb * KB_DIMS + grp * VEC + e; }
+    __device__ __forceinline__ static acc_t mma(vec_t a, vec_t b, int, acc_t c) {
+        return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
+    }
+};
+
+// bf16: v_mfma_f32_16x16x32_bf16 (gfx950), same layout as fp16.
+template <>
+struct Mfma<__bf16, 16> {
+    static constexpr int TM = 16, GROUPS = 4, VEC = 8;
+    static constexpr int KS_PER_KB = 1, KB_DIMS = 32, ACC = 4, NB = EXEMCL_NB16;
+    using acc_t = f32x4;
+    using vec_t = bf16x8;
+    using elem_t = __bf16;
+    __device__ __forceinline__ static int dim(int kb, int grp, int e) { return kb * KB_DIMS + grp * VEC + e; }
+    __device__ __forceinline__ static acc_t mma(vec_t a, vec_t b, int, acc_t c) {
+        return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
     }
 };
 

@@ -83,7 +83,7 @@ bool layout_eval(int64_t n, int64_t d, int64_t l, int64_t k, int precision, int 
         L->gpc = (L->ngroups + chunks - 1) / chunks;
         L->off_partials = 0;
         L->off_tiles = align_up(L->G * L->lpad * 4, 256);
-        L->bytes = align_up(L->off_tiles + L->ngroups * k * tile_bytes(L->mp), 256);
+        L->bytes = align_up(L->off_tiles + L->ngroups * mfma_tiles_per_group(L->mp, k) * tile_bytes(L->mp), 256);
         return true;
     }
     if (path == EXEMCL_PATH_VALU) {
@@ -241,8 +241,8 @@ hipError_t run_chunk(const Layout &L, char *base, const void *V, int64_t n, int6
         e = launch_pack(precision, L.mp, rows->V, n, (int)rows->ld, sets, l, k, tiles, st);
         if (e == hipSuccess) {
             ProfRange pr(st);
-            e = launch_mfma(precision, MODE_SUM, L.mp, rows->V, n, (int)rows->ld, tiles, k, L.ngroups, L.gpc, m0, partials,
-                            L.lpad, nullptr, st);
+            e = launch_mfma(precision, MODE_SUM, L.mp, rows->V, n, (int)rows->ld, tiles, mfma_tiles_per_group(L.mp, k),
+                            L.ngroups, L.gpc, m0, partials, L.lpad, nullptr, st);
             pr.end();
         }
     } else if (L.path == EXEMCL_PATH_VALU) {

@@ -23,6 +23,7 @@ struct MfmaPlan {
     int waves;      // wavefronts per workgroup
     int rows;       // rows per workgroup = waves * rt * tile
     int kb_dims;    // coordinates per k-block
+    int nb;         // set members per staged tile (a set group spans ceil(k / nb) tiles)
 };
 
 bool mfma_plan(int prec, int64_t d, MfmaPlan *p);
@@ -33,7 +34,7 @@ struct MfmaArgs {
     int64_t n;
     int ld;  // row stride in elements: rows are whole 16-byte lane vectors
     const void *tiles;
-    int64_t k, ngroups, gpc;
+    int64_t kt, ngroups, gpc;  // staged tiles per set group, set groups, groups per chunk
     const float *m0;
     float *partials;
     int64_t lpad;
@@ -71,25 +72,29 @@ bool mfma_rows_ready(int prec, const void *V, int64_t d);
 // Vp[i][t] = V[i][t] for t < d, 0 for d <= t < ld (n rows).
 hipError_t launch_pad(int prec, const void *V, int64_t n, int d, void *Vp, int ld, hipStream_t st);
 
-// Stage the exemplar tiles of `l` sets of `k` indices: for every (set group,
-// slot) pair one TM-column tile holding TM biases -||s||^2/2 (-FLT_MAX for
-// padding columns and invalid indices) and the B lane vectors.
+// Stage the exemplar tiles of `l` sets of `k` indices: for every set group,
+// ceil(k / nb) tiles, each holding members q*nb .. q*nb+nb-1 of the group's
+// TM sets as nb column groups: TM*nb biases -||s||^2/2 (-FLT_MAX for padding
+// columns, members past k and invalid indices) and the B lane vectors.
 hipError_t launch_pack(int prec, const MfmaPlan &pl, const void *V, int64_t n, int ld, const int32_t *sets,
                        int64_t l, int64_t k, void *tiles, hipStream_t st);
 
-// Bytes of one staged tile (bias header + B lane vectors).
+// Bytes of one staged tile (bias header + B lane vectors), and staged tiles
+// per set group of k members.
 int64_t mfma_tile_bytes(const MfmaPlan &pl);
+int64_t mfma_tiles_per_group(const MfmaPlan &pl, int64_t k);
 
 // Mode of the MFMA kernel's epilogue.
 enum Mode { MODE_SUM = 0, MODE_ROWMAX = 1 };
 
+// `kt` = staged tiles per set group (mfma_tiles_per_group).
 // partials[(rb * waves + w) * lpad + j] = sum over the rows of wavefront w
 // of row block rb of max(m0(v), max_p (<v, s_jp> - ||s_jp||^2 / 2)); m0 = 0
 // when null (fp32 only otherwise).  MODE_ROWMAX (fp32, groups_per_chunk =
 // ngroups) instead writes rowmax[v] = max(m0(v), 0, max over all staged
 // columns); rowmax must not alias m0.
 hipError_t launch_mfma(int prec, int mode, const MfmaPlan &pl, const void *V, int64_t n, int ld,
-                       const void *tiles, int64_t k, int64_t ngroups, int64_t groups_per_chunk,
+                       const void *tiles, int64_t kt, int64_t ngroups, int64_t groups_per_chunk,
                        const float *m0, float *partials, int64_t lpad, float *rowmax, hipStream_t st);
 
 hipError_t launch_valu(int prec, const ValuPlan &pl, const void *V, int64_t n, int d, const int32_t *sets,

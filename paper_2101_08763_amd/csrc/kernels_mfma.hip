@@ -6,6 +6,11 @@
 #include "internal.h"
 #include "mfma_kernels.hpp"
 
+// fp16/bf16 rows of at least this many coordinates use the 16x16x32 shape.
+#ifndef EXEMCL_F16_WIDE_D
+#define EXEMCL_F16_WIDE_D 17
+#endif
+
 namespace exemcl {
 
 // k-block counts with a compiled kernel; d is zero-padded up to the next one.
@@ -21,36 +26,47 @@ bool mfma_plan(int prec, int64_t d, MfmaPlan *p) {
     if (d < 1 || d > 512) return false;
     MfmaPlan q{};
     q.waves = 4;
+    q.nb = 1;
     if (prec == P_FP32 && d <= 256) {
         // v_mfma_f32_32x32x2_f32, 8 coordinates per k-block
         q.tile = 32;
         q.kb_dims = 8;
         q.nkb = bucket((int)((d + 7) / 8));
         q.nks_last = q.nkb == 1 ? (int)(d < 4 ? d : 4) : 4;  // instruction e covers dims e and 4 + e
-        q.rt = q.nkb <= EXEMCL_RT1_NKB32 ? 1 : q.nkb <= 16 ? 2 : 1;  // as rt_small<float, NKB>()
     } else if (prec == P_FP32) {
         // v_mfma_f32_16x16x4_f32, 16 coordinates per k-block
         q.tile = 16;
         q.kb_dims = 16;
         q.nkb = bucket((int)((d + 15) / 16));
         q.nks_last = 4;
-        q.rt = 1;
+    } else if (d >= EXEMCL_F16_WIDE_D) {
+        // v_mfma_f32_16x16x32_{f16,bf16}, 32 coordinates per k-block, two
+        // set members per tile
+        q.tile = 16;
+        q.kb_dims = 32;
+        q.nkb = bucket((int)((d + 31) / 32));
+        q.nks_last = 1;
+        q.nb = EXEMCL_NB16;
     } else {
-        // v_mfma_f32_32x32x16_{f16,bf16}, 16 coordinates per k-block
+        // v_mfma_f32_32x32x16_{f16,bf16}, 16 coordinates per k-block (one
+        // k-block for d <= 16, where 32-coordinate blocks would be half padding)
         q.tile = 32;
         q.kb_dims = 16;
         q.nkb = bucket((int)((d + 15) / 16));
         q.nks_last = 1;
-        q.rt = q.nkb <= 16 ? 2 : 1;
     }
     if (q.nkb < 1) return false;
-    q.waves = q.nkb <= EXEMCL_BIG_NKB ? EXEMCL_SMALL_WAVES : EXEMCL_BIG_WAVES;  // as waves_for<NKB>()
+    const int eb = prec == P_FP32 ? 4 : 2;
+    q.rt = plan_rt(eb, q.tile, q.nkb);
+    q.waves = plan_waves(eb, q.tile, q.nkb);
     q.rows = q.waves * q.rt * q.tile;
     *p = q;
     return true;
 }
 
-int64_t mfma_tile_bytes(const MfmaPlan &pl) { return HDR + (int64_t)pl.nkb * 1024; }
+int64_t mfma_tile_bytes(const MfmaPlan &pl) { return HDR + (int64_t)pl.nkb * pl.nb * 1024; }
+
+int64_t mfma_tiles_per_group(const MfmaPlan &pl, int64_t k) { return (k + pl.nb - 1) / pl.nb; }
 
 hipError_t launch_pack(int prec, const MfmaPlan &pl, const void *V, int64_t n, int ld, const int32_t *sets,
                        int64_t l, int64_t k, void *tiles, hipStream_t st) {
@@ -63,9 +79,9 @@ hipError_t launch_pack(int prec, const MfmaPlan &pl, const void *V, int64_t n, i
 }
 
 hipError_t launch_mfma(int prec, int mode, const MfmaPlan &pl, const void *V, int64_t n, int ld, const void *tiles,
-                       int64_t k, int64_t ngroups, int64_t gpc, const float *m0, float *partials, int64_t lpad,
+                       int64_t kt, int64_t ngroups, int64_t gpc, const float *m0, float *partials, int64_t lpad,
                        float *rowmax, hipStream_t st) {
-    const MfmaArgs x{V, n, ld, tiles, k, ngroups, gpc, m0, partials, lpad, rowmax};
+    const MfmaArgs x{V, n, ld, tiles, kt, ngroups, gpc, m0, partials, lpad, rowmax};
     switch (prec) {
     case P_FP32: return eval_run_f32(pl, mode, x, st);
     case P_FP16: return mode == MODE_SUM ? eval_run_f16(pl, mode, x, st) : hipErrorInvalidValue;

@@ -36,7 +36,7 @@
 
 namespace exemcl {
 
-constexpr int HDR = 128;  // tile header: TM fp32 biases, padded to 128 bytes
+constexpr int HDR = 128;  // tile header: TM * NB fp32 biases, padded to 128 bytes
 
 template <int NKB>
 constexpr int tile_bytes_of() {
@@ -46,47 +46,56 @@ constexpr int tile_bytes_of() {
 // ---------------------------------------------------------------------------
 // Staging: gather exemplar rows by index into tiles, with their norms.
 //
-// Tile t = g*k + p holds, for the TM sets g*TM .. g*TM+TM-1, their member p.
-// Byte layout of one tile (HDR + nkb * 1024 bytes):
-//   [0, HDR)               TM fp32 biases -||s||^2/2, one per column
-//   [HDR + kb*1024 + 16*L)  lane L's 16-byte B-operand vector for k-block kb
-// Padding columns (set >= l), empty slots and invalid indices become zero
-// vectors with bias -FLT_MAX, which never wins the running max.
-// Rows are ld elements, zero past the data's d.  One wavefront per tile;
-// ||s||^2 is summed
-// from the lane vectors (fp32, k-blocks then elements in order, then the
-// K-groups of the column with a fixed xor tree).
+// A set group (TM consecutive sets) spans kt = ceil(k / NB) tiles; tile
+// t = g*kt + q holds members q*NB .. q*NB+NB-1 of the sets g*TM .. g*TM+TM-1,
+// member q*NB + h in column group h.  Byte layout of one tile
+// (HDR + nkb * NB * 1024 bytes):
+//   [0, HDR)                         TM*NB fp32 biases -||s||^2/2, column
+//                                    c of group h at index h*TM + c
+//   [HDR + (kb*NB + h)*1024 + 16*L)  lane L's 16-byte B-operand vector for
+//                                    k-block kb of column group h
+// Padding columns (set >= l), members past k, empty slots and invalid
+// indices become zero vectors with bias -FLT_MAX, which never wins the
+// running max.  Rows are ld elements, zero past the data's d.  One wavefront
+// per tile; ||s||^2 is summed from the lane vectors (fp32, k-blocks then
+// elements in order, then the K-groups of the column with a fixed xor tree).
 // ---------------------------------------------------------------------------
 template <typename T, int TILE>
 __global__ __launch_bounds__(64) void pack_tiles_kernel(const T *__restrict__ V, int64_t n, int ld,
                                                         const int32_t *__restrict__ sets, int64_t l,
                                                         int64_t k, int nkb, unsigned char *__restrict__ tiles) {
     using M = Mfma<T, TILE>;
+    constexpr int NB = M::NB;
+    const int64_t kt = (k + NB - 1) / NB;
     const int64_t t = blockIdx.x;
-    const int64_t g = t / k, p = t - (t / k) * k;
+    const int64_t g = t / kt, q = t - (t / kt) * kt;
     const int lane = threadIdx.x;
     const int col = lane % M::TM, grp = lane / M::TM;
     const int64_t j = g * M::TM + col;
-    int64_t idx = -1;
-    if (j < l) idx = sets[j * k + p];
-    const bool valid = idx >= 0 && idx < n;
-    unsigned char *tile = tiles + t * (int64_t)(HDR + nkb * 1024);
+    unsigned char *tile = tiles + t * (int64_t)(HDR + nkb * NB * 1024);
     typename M::vec_t *dst = reinterpret_cast<typename M::vec_t *>(tile + HDR);
-    const int64_t r = valid ? idx : n;  // row n reads as zeros
-    float q = 0.0f;
-    for (int kb = 0; kb < nkb; ++kb) {
-        const typename M::vec_t v =
-            lanevec_keep<M>(lanevec_raw<M>(V, n, ld, r, kb, grp), lanevec_live<M>(n, ld, r, kb, grp));
-        dst[kb * 64 + lane] = v;
 #pragma unroll
-        for (int e = 0; e < M::VEC; ++e) {
-            const float x = to_f32(v[e]);
-            q = fmaf(x, x, q);
+    for (int h = 0; h < NB; ++h) {
+        const int64_t p = q * NB + h;
+        int64_t idx = -1;
+        if (j < l && p < k) idx = sets[j * k + p];
+        const bool valid = idx >= 0 && idx < n;
+        const int64_t r = valid ? idx : n;  // row n reads as zeros
+        float sq = 0.0f;
+        for (int kb = 0; kb < nkb; ++kb) {
+            const typename M::vec_t v =
+                lanevec_keep<M>(lanevec_raw<M>(V, n, ld, r, kb, grp), lanevec_live<M>(n, ld, r, kb, grp));
+            dst[(kb * NB + h) * 64 + lane] = v;
+#pragma unroll
+            for (int e = 0; e < M::VEC; ++e) {
+                const float x = to_f32(v[e]);
+                sq = fmaf(x, x, sq);
+            }
         }
-    }
 #pragma unroll
-    for (int off = M::TM; off < 64; off <<= 1) q += __shfl_xor(q, off);
-    if (grp == 0) reinterpret_cast<float *>(tile)[col] = valid ? -0.5f * q : -FLT_MAX;
+        for (int off = M::TM; off < 64; off <<= 1) sq += __shfl_xor(sq, off);
+        if (grp == 0) reinterpret_cast<float *>(tile)[h * M::TM + col] = valid ? -0.5f * sq : -FLT_MAX;
+    }
 }
 
 // Stage geometry, fixed at compile time per k-block bucket.  Workgroups of
@@ -99,6 +108,18 @@ __global__ __launch_bounds__(64) void pack_tiles_kernel(const T *__restrict__ V,
 // a tile, up to EXEMCL_PF B fragments are read from LDS ahead of their use.
 #ifndef EXEMCL_PF
 #define EXEMCL_PF 3
+#endif
+#ifndef EXEMCL_PF_SCHED
+#define EXEMCL_PF_SCHED 4
+#endif
+#ifndef EXEMCL_SCHED_MIN_NF
+#define EXEMCL_SCHED_MIN_NF 16
+#endif
+#ifndef EXEMCL_SCHED16
+#define EXEMCL_SCHED16 1
+#endif
+#ifndef EXEMCL_SCHED32
+#define EXEMCL_SCHED32 0
 #endif
 #ifndef EXEMCL_PAIR
 #define EXEMCL_PAIR 1
@@ -117,6 +138,27 @@ __global__ __launch_bounds__(64) void pack_tiles_kernel(const T *__restrict__ V,
 #endif
 #ifndef EXEMCL_BIG_WAVES
 #define EXEMCL_BIG_WAVES 8
+#endif
+#ifndef EXEMCL_RT16_SMALL
+#define EXEMCL_RT16_SMALL 2
+#endif
+#ifndef EXEMCL_RT16_MID
+#define EXEMCL_RT16_MID 2
+#endif
+#ifndef EXEMCL_RT16_BIG
+#define EXEMCL_RT16_BIG 1
+#endif
+#ifndef EXEMCL_RT16X16_NKB
+#define EXEMCL_RT16X16_NKB 8
+#endif
+#ifndef EXEMCL_RT16X16_SMALL
+#define EXEMCL_RT16X16_SMALL 4
+#endif
+#ifndef EXEMCL_RT16X16_BIG
+#define EXEMCL_RT16X16_BIG 2
+#endif
+#ifndef EXEMCL_WAVES16_BIG
+#define EXEMCL_WAVES16_BIG EXEMCL_BIG_WAVES
 #endif
 #ifndef EXEMCL_BIG_NKB
 #define EXEMCL_BIG_NKB 8
@@ -141,11 +183,19 @@ constexpr int round_stage(int bytes) {
     return (bytes + WAVES * 1024 - 1) / (WAVES * 1024) * (WAVES * 1024);
 }
 
+// LDS one workgroup's ring may use: workgroups of at most 4 wavefronts (one
+// per SIMD) leave room for a second workgroup on the CU, so that each SIMD
+// can interleave two wavefronts.
+template <int WAVES>
+constexpr int lds_budget() {
+    return WAVES <= 4 ? kLdsBytes / 2 : kLdsBytes;
+}
+
 template <int NKB, int WAVES>
 constexpr int tiles_per_stage() {
     constexpr int tb = tile_bytes_of<NKB>();
     int tps = NKB <= EXEMCL_BIG_NKB ? (EXEMCL_STAGE_MIN / tb > 1 ? EXEMCL_STAGE_MIN / tb : 1) : EXEMCL_TPS_BIG;
-    while (tps > 1 && 2 * round_stage<NKB, WAVES>(tps * tb) > kLdsBytes) --tps;
+    while (tps > 1 && 2 * round_stage<NKB, WAVES>(tps * tb) > lds_budget<WAVES>()) --tps;
     return tps;
 }
 
@@ -157,8 +207,18 @@ constexpr int stage_bytes() {
 template <int NKB, int WAVES>
 constexpr int ring_depth() {
     constexpr int want = NKB <= EXEMCL_BIG_NKB ? EXEMCL_RING_SMALL : EXEMCL_RING_BIG;
-    constexpr int fit = kLdsBytes / stage_bytes<NKB, WAVES>();
+    constexpr int fit = (stage_bytes<NKB, WAVES>() * 2 <= lds_budget<WAVES>() ? lds_budget<WAVES>() : kLdsBytes) /
+                        stage_bytes<NKB, WAVES>();
     return want < fit ? want : fit;
+}
+
+// Prefetch depth for reads that run across tiles: the largest divisor of
+// nkb not above `want`; when that is 1, all nkb fragments of a short tile.
+constexpr int prefetch_depth(int nkb, int want) {
+    int best = 1;
+    for (int p = 2; p <= want && p <= nkb; ++p)
+        if (nkb % p == 0) best = p;
+    return (best == 1 && nkb <= 2 * want + 1) ? nkb : best;
 }
 
 template <int N>
@@ -193,7 +253,7 @@ __device__ __forceinline__ void wait_vmcnt() {
 // ---------------------------------------------------------------------------
 template <typename T, int TILE, int NKB, int NKS_LAST, int RT, int WAVES, int MODE, bool HAS_M0>
 __global__ __launch_bounds__(WAVES * 64) void eval_mfma_kernel(const T *__restrict__ V, int64_t n, int ld,
-                                                                 const unsigned char *__restrict__ tiles, int64_t k,
+                                                                 const unsigned char *__restrict__ tiles, int64_t kt,
                                                                  int64_t ngroups, int64_t gpc,
                                                                  const float *__restrict__ m0,
                                                                  float *__restrict__ partials, int64_t lpad,
@@ -202,14 +262,25 @@ __global__ __launch_bounds__(WAVES * 64) void eval_mfma_kernel(const T *__restri
     using vec_t = typename M::vec_t;
     using acc_t = typename M::acc_t;
     constexpr int TM = M::TM;
+    constexpr int NB = M::NB;     // column groups (set members) per tile
+    constexpr int NF = NKB * NB;  // B fragments per tile, fragment f = kb * NB + h
     constexpr int NT = WAVES * 64;
-    constexpr int TB = tile_bytes_of<NKB>();
-    constexpr int SB = stage_bytes<NKB, WAVES>();
-    constexpr int TPS = tiles_per_stage<NKB, WAVES>();
+    constexpr int TB = tile_bytes_of<NF>();
+    constexpr int SB = stage_bytes<NF, WAVES>();
+    constexpr int TPS = tiles_per_stage<NF, WAVES>();
     constexpr int CNT = SB / (NT * 16);
-    constexpr int NBUF = ring_depth<NKB, WAVES>();
-    constexpr int PF = NKB < EXEMCL_PF ? NKB : EXEMCL_PF;  // B fragments in flight ahead of use
-    constexpr bool PAIR = EXEMCL_PAIR && NKB <= (sizeof(T) == 4 ? EXEMCL_PAIR_NKB32 : EXEMCL_PAIR_NKB16);
+    constexpr int NBUF = ring_depth<NF, WAVES>();
+    // Reads across tiles pay off for long tiles; short ones keep the registers
+    // for a third wavefront per SIMD instead.
+    constexpr bool SCHED = (sizeof(T) == 4 ? EXEMCL_SCHED32 : EXEMCL_SCHED16) && NF >= EXEMCL_SCHED_MIN_NF;
+    // B fragments in flight ahead of use.  When the reads run across tiles
+    // (SCHED) the ring of PF slots must wrap exactly at a tile's end, so PF
+    // divides NF; the next tile then finds fragment i in slot i.
+    constexpr int PF = SCHED ? prefetch_depth(NF, EXEMCL_PF_SCHED) : (NF < EXEMCL_PF ? NF : EXEMCL_PF);
+    static_assert(!SCHED || NF % PF == 0, "cross-tile prefetch ring must wrap at the tile end");
+    static_assert(TM * NB * 4 <= HDR, "tile header holds every column's bias");
+    static_assert(MODE == MODE_SUM || NB == 1, "the row-max mode stages one member per tile");
+    constexpr bool PAIR = EXEMCL_PAIR && NB == 1 && NKB <= (sizeof(T) == 4 ? EXEMCL_PAIR_NKB32 : EXEMCL_PAIR_NKB16);
     static_assert(TPS >= 1 && TPS * TB <= SB && NBUF >= 2 && NBUF * SB <= kLdsBytes, "stage geometry");
     static_assert(CNT * (NBUF - 2) < 64, "vmcnt range");
     static_assert(NKS_LAST >= 1 && NKS_LAST <= M::KS_PER_KB, "k-steps of the last block");
@@ -224,9 +295,9 @@ __global__ __launch_bounds__(WAVES * 64) void eval_mfma_kernel(const T *__restri
     const int64_t g1 = min(ngroups, g0 + gpc);
     const int64_t row0 = rb * (int64_t)(WAVES * RT * TM) + (int64_t)wave * RT * TM;
 
-    const int64_t ntiles = (g1 - g0) * k;
+    const int64_t ntiles = (g1 - g0) * kt;
     const int64_t nstages = (ntiles + TPS - 1) / TPS;
-    const unsigned char *chunk = tiles + g0 * k * (int64_t)TB;
+    const unsigned char *chunk = tiles + g0 * kt * (int64_t)TB;
     const int64_t chunk_bytes = ntiles * (int64_t)TB;
 
     // Queue the direct-to-LDS copy of stage s (CNT 16-byte loads per thread).
@@ -287,88 +358,171 @@ __global__ __launch_bounds__(WAVES * 64) void eval_mfma_kernel(const T *__restri
 #pragma unroll
         for (int i = 0; i < M::ACC; ++i) m[rt][i] = m_init(rt, i);
 
-    // One tile: the bias enters as the accumulators' initial value (fp32),
-    // then the branch-free MFMA chain over the NKB k-blocks, B fragments read
-    // from LDS up to PF ahead of use.
-    auto chain = [&](const unsigned char *tb, acc_t (&acc)[RT]) {
+    // One tile: each column group's bias enters as its accumulators' initial
+    // value (fp32), then the branch-free MFMA chain over the NKB k-blocks.
+    // B fragments are software-pipelined: bq holds the next PF fragments in
+    // use order, and each use reads the fragment PF positions ahead -- past
+    // the end of this tile that is the start of `tnext` (the following tile
+    // of the same stage, or this tile again for the last one: a harmless
+    // re-read), whose biases are read with its first fragment.  With SCHED
+    // the compiler may not move instructions across k-block boundaries, so
+    // the reads stay ahead of their use instead of being sunk next to it;
+    // without it every tile starts its own reads (no reads across tiles).
+    auto fence = [&]() {
+        if constexpr (SCHED) __builtin_amdgcn_sched_barrier(0);
+    };
+    auto head = [&](const unsigned char *tb, vec_t (&bq)[PF], float (&bias)[NB]) {
         const vec_t *B = reinterpret_cast<const vec_t *>(tb + HDR);
-        vec_t bq[PF];
 #pragma unroll
         for (int i = 0; i < PF; ++i) bq[i] = B[i * 64 + lane];
-        const float b = reinterpret_cast<const float *>(tb)[lr];
+#pragma unroll
+        for (int h = 0; h < NB; ++h) bias[h] = reinterpret_cast<const float *>(tb)[h * TM + lr];
+    };
+    auto chain = [&](const unsigned char *tb, const unsigned char *tnext, vec_t (&bq)[PF], float (&bias)[NB],
+                     acc_t (&acc)[RT][NB]) {
+        if constexpr (!SCHED) head(tb, bq, bias);
+        const vec_t *B = reinterpret_cast<const vec_t *>(tb + HDR);
+        const vec_t *Bn = reinterpret_cast<const vec_t *>(tnext + HDR);
 #pragma unroll
         for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
-            for (int i = 0; i < M::ACC; ++i) acc[rt][i] = b;
+            for (int h = 0; h < NB; ++h)
+#pragma unroll
+                for (int i = 0; i < M::ACC; ++i) acc[rt][h][i] = bias[h];
+        float bias_next[NB];
+#pragma unroll
+        for (int h = 0; h < NB; ++h) bias_next[h] = 0.0f;
 #pragma unroll
         for (int kb = 0; kb < NKB; ++kb) {
-            const vec_t bv = bq[kb % PF];
-            if (kb + PF < NKB) bq[kb % PF] = B[(kb + PF) * 64 + lane];
+            vec_t bv[NB];
+#pragma unroll
+            for (int h = 0; h < NB; ++h) {
+                const int f = kb * NB + h;
+                bv[h] = bq[f % PF];
+                const int ahead = f + PF;
+                if (ahead < NF) {
+                    bq[f % PF] = B[ahead * 64 + lane];
+                } else if constexpr (SCHED) {
+                    bq[f % PF] = Bn[(ahead - NF) * 64 + lane];
+                    if (ahead == NF) {
+#pragma unroll
+                        for (int hh = 0; hh < NB; ++hh)
+                            bias_next[hh] = reinterpret_cast<const float *>(tnext)[hh * TM + lr];
+                    }
+                }
+            }
+            fence();
 #pragma unroll
             for (int e = 0; e < M::KS_PER_KB; ++e) {
                 if (kb < NKB - 1 || e < NKS_LAST) {
 #pragma unroll
-                    for (int rt = 0; rt < RT; ++rt) acc[rt] = M::mma(a[rt][kb], bv, e, acc[rt]);
+                    for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+                        for (int h = 0; h < NB; ++h) acc[rt][h] = M::mma(a[rt][kb], bv[h], e, acc[rt][h]);
                 }
             }
+            fence();
+        }
+        if constexpr (SCHED) {
+#pragma unroll
+            for (int h = 0; h < NB; ++h) bias[h] = bias_next[h];
         }
     };
+    // m = max(m, every column group of x): with NB = 2 one max3 per element.
+    // A set group's first tile folds against the initial value instead, so
+    // the running max needs no reset between groups (MODE_SUM; MODE_ROWMAX
+    // keeps one running max over everything staged).
+    auto fold_from = [&](const acc_t (&x)[RT][NB], auto start) {
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+            for (int i = 0; i < M::ACC; ++i) {
+                float v = start(rt, i);
+#pragma unroll
+                for (int h = 0; h < NB; ++h) v = fmaxf(v, x[rt][h][i]);
+                m[rt][i] = v;
+            }
+    };
+    auto fold = [&](const acc_t (&x)[RT][NB], bool first) {
+        if (first) fold_from(x, m_init);  // uniform branch: two straight-line variants
+        else fold_from(x, [&](int rt, int i) { return m[rt][i]; });
+    };
+    // Two single-member tiles of the same set group (NB = 1): one max3.
+    auto fold2_from = [&](const acc_t (&x)[RT][NB], const acc_t (&y)[RT][NB], auto start) {
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+            for (int i = 0; i < M::ACC; ++i) m[rt][i] = fmaxf(fmaxf(start(rt, i), x[rt][0][i]), y[rt][0][i]);
+    };
+    // Sum of this lane's running maxima in a fixed pairwise order.
+    auto lane_sum = [&]() {
+        constexpr int NV = RT * M::ACC;
+        static_assert((NV & (NV - 1)) == 0, "pairwise sum over a power of two");
+        float v[NV];
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+            for (int i = 0; i < M::ACC; ++i) v[rt * M::ACC + i] = m[rt][i];
+#pragma unroll
+        for (int w = NV / 2; w >= 1; w /= 2)
+#pragma unroll
+            for (int i = 0; i < w; ++i) v[i] += v[i + w];
+        return v[0];
+    };
 
+    // Set-group and member counters fit 32 bits (ngroups * TM <= lpad, a
+    // partial-sum row of fp32 values); keeping them 32-bit keeps them in
+    // scalar registers.
+    const int ktile = (int)kt;
     float *wpart = partials + (rb * WAVES + wave) * lpad;
-    int64_t g = g0;
-    int64_t p = 0;
-    for (int64_t s = 0; s < nstages; ++s) {
-        if (s + NBUF - 2 < nstages) wait_vmcnt<CNT * (NBUF - 2)>();
+    int g = (int)g0;
+    int p = 0;
+    const int nst = (int)nstages;
+    for (int s = 0; s < nst; ++s) {
+        if (s + NBUF - 2 < nst) wait_vmcnt<CNT * (NBUF - 2)>();
         else wait_vmcnt<0>();
         __syncthreads();
-        if (s + NBUF - 1 < nstages) issue(s + NBUF - 1);
+        if (s + NBUF - 1 < nst) issue(s + NBUF - 1);
 
-        const unsigned char *buf = smem + (int)(s % NBUF) * SB;
-        const int tn = (int)min((int64_t)TPS, ntiles - s * TPS);
-        // Close set group g after its last member: sum this lane's rows for
+        const unsigned char *buf = smem + (s % NBUF) * SB;
+        const int tn = (int)min((int64_t)TPS, ntiles - (int64_t)s * TPS);
+        auto tile_at = [&](int i) { return buf + (i < tn ? i : tn - 1) * TB; };
+        vec_t bq[PF];
+        float bias[NB];
+#pragma unroll
+        for (int h = 0; h < NB; ++h) bias[h] = 0.0f;
+        if constexpr (SCHED) head(buf, bq, bias);
+        // Close set group g after its last tile: sum this lane's rows for
         // its column, then the K-groups holding the other rows of the same
-        // column, and restart the running max.
+        // column.
         auto group_end = [&]() {
             if constexpr (MODE == MODE_SUM) {
-                float sum = 0.0f;
-#pragma unroll
-                for (int rt = 0; rt < RT; ++rt)
-#pragma unroll
-                    for (int i = 0; i < M::ACC; ++i) sum += m[rt][i];
+                float sum = lane_sum();
 #pragma unroll
                 for (int off = TM; off < 64; off <<= 1) sum += __shfl_xor(sum, off);
-                if (grp == 0) wpart[g * TM + lr] = sum;
-#pragma unroll
-                for (int rt = 0; rt < RT; ++rt)
-#pragma unroll
-                    for (int i = 0; i < M::ACC; ++i) m[rt][i] = m_init(rt, i);
+                if (grp == 0) wpart[(int64_t)g * TM + lr] = sum;
             }
         };
         if constexpr (PAIR) {
             int tt = 0;
             while (tt < tn) {
-                if (tt + 1 < tn && p + 1 < k) {
+                if (tt + 1 < tn && p + 1 < ktile) {
                     // Two members of the same set group: one max3 per element.
-                    acc_t x[RT], y[RT];
-                    chain(buf + tt * TB, x);
-                    chain(buf + (tt + 1) * TB, y);
-#pragma unroll
-                    for (int rt = 0; rt < RT; ++rt)
-#pragma unroll
-                        for (int i = 0; i < M::ACC; ++i) m[rt][i] = fmaxf(fmaxf(m[rt][i], x[rt][i]), y[rt][i]);
+                    acc_t x[RT][NB], y[RT][NB];
+                    chain(tile_at(tt), tile_at(tt + 1), bq, bias, x);
+                    chain(tile_at(tt + 1), tile_at(tt + 2), bq, bias, y);
+                    if (MODE == MODE_SUM && p == 0) fold2_from(x, y, m_init);
+                    else fold2_from(x, y, [&](int rt, int i) { return m[rt][i]; });
                     tt += 2;
                     p += 2;
                 } else {
-                    acc_t x[RT];
-                    chain(buf + tt * TB, x);
-#pragma unroll
-                    for (int rt = 0; rt < RT; ++rt)
-#pragma unroll
-                        for (int i = 0; i < M::ACC; ++i) m[rt][i] = fmaxf(m[rt][i], x[rt][i]);
+                    acc_t x[RT][NB];
+                    chain(tile_at(tt), tile_at(tt + 1), bq, bias, x);
+                    fold(x, MODE == MODE_SUM && p == 0);
                     tt += 1;
                     p += 1;
                 }
-                if (p == k) {
+                if (p == ktile) {
                     group_end();
                     p = 0;
                     ++g;
@@ -376,14 +530,11 @@ __global__ __launch_bounds__(WAVES * 64) void eval_mfma_kernel(const T *__restri
             }
         } else {
             for (int tt = 0; tt < tn; ++tt) {
-                acc_t x[RT];
-                chain(buf + tt * TB, x);
-#pragma unroll
-                for (int rt = 0; rt < RT; ++rt)
-#pragma unroll
-                    for (int i = 0; i < M::ACC; ++i) m[rt][i] = fmaxf(m[rt][i], x[rt][i]);
-                if (p == k - 1) group_end();
-                if (++p == k) {
+                acc_t x[RT][NB];
+                chain(tile_at(tt), tile_at(tt + 1), bq, bias, x);
+                fold(x, MODE == MODE_SUM && p == 0);
+                if (++p == ktile) {
+                    group_end();
                     p = 0;
                     ++g;
                 }
@@ -422,15 +573,17 @@ template <typename T, int TILE>
 hipError_t pack_launch(const MfmaPlan &pl, const void *V, int64_t n, int ld, const int32_t *sets, int64_t l,
                        int64_t k, void *tiles, hipStream_t st) {
     const int64_t ngroups = (l + TILE - 1) / TILE;
-    hipLaunchKernelGGL((pack_tiles_kernel<T, TILE>), dim3((unsigned)(ngroups * k)), dim3(64), 0, st,
+    const int64_t kt = (k + Mfma<T, TILE>::NB - 1) / Mfma<T, TILE>::NB;
+    hipLaunchKernelGGL((pack_tiles_kernel<T, TILE>), dim3((unsigned)(ngroups * kt)), dim3(64), 0, st,
                        (const T *)V, n, ld, sets, l, k, pl.nkb, (unsigned char *)tiles);
     return hipGetLastError();
 }
 
 template <typename T, int TILE, int NKB, int NKS_LAST, int RT, int WAVES, int MODE, bool HAS_M0>
 hipError_t eval_launch_t(const MfmaArgs &x, hipStream_t st) {
-    constexpr int SB = stage_bytes<NKB, WAVES>();
-    constexpr int NBUF = ring_depth<NKB, WAVES>();
+    constexpr int NF = NKB * Mfma<T, TILE>::NB;
+    constexpr int SB = stage_bytes<NF, WAVES>();
+    constexpr int NBUF = ring_depth<NF, WAVES>();
     auto kern = eval_mfma_kernel<T, TILE, NKB, NKS_LAST, RT, WAVES, MODE, HAS_M0>;
     const size_t lds = (size_t)NBUF * SB;
     if (lds > 64 * 1024) {
@@ -441,7 +594,7 @@ hipError_t eval_launch_t(const MfmaArgs &x, hipStream_t st) {
     const int64_t G = (x.n + rows - 1) / rows;
     const int64_t chunks = (x.ngroups + x.gpc - 1) / x.gpc;
     hipLaunchKernelGGL(kern, dim3((unsigned)G, (unsigned)chunks), dim3(WAVES * 64), lds, st, (const T *)x.V, x.n,
-                       x.ld, (const unsigned char *)x.tiles, x.k, x.ngroups, x.gpc, x.m0, x.partials, x.lpad,
+                       x.ld, (const unsigned char *)x.tiles, x.kt, x.ngroups, x.gpc, x.m0, x.partials, x.lpad,
                        x.rowmax);
     return hipGetLastError();
 }
@@ -454,61 +607,78 @@ hipError_t eval_launch(const MfmaArgs &x, hipStream_t st) {
     return eval_launch_t<T, TILE, NKB, NKS_LAST, RT, WAVES, MODE, false>(x, st);
 }
 
-// Wavefronts per workgroup for a k-block bucket (the plan uses the same rule).
-template <int NKB>
-constexpr int waves_for() {
-    return NKB <= EXEMCL_BIG_NKB ? EXEMCL_SMALL_WAVES : EXEMCL_BIG_WAVES;
+// Row tiles per wavefront and wavefronts per workgroup for a k-block bucket,
+// as functions of (element bytes, tile, k-blocks) so that the host-side plan
+// (mfma_plan) and the compiled instantiations follow one rule.
+constexpr int plan_rt(int elem_bytes, int tile, int nkb) {
+    if (tile == 16) return elem_bytes == 4 ? 1 : nkb <= EXEMCL_RT16X16_NKB ? EXEMCL_RT16X16_SMALL : EXEMCL_RT16X16_BIG;
+    if (elem_bytes == 4) return nkb <= EXEMCL_RT1_NKB32 ? 1 : nkb <= 16 ? 2 : 1;
+    return nkb <= EXEMCL_BIG_NKB ? EXEMCL_RT16_SMALL : nkb <= 16 ? EXEMCL_RT16_MID : EXEMCL_RT16_BIG;
 }
 
-// Row tiles per wavefront for buckets up to 16 k-blocks: 2, except fp32
-// buckets up to EXEMCL_RT1_NKB32 k-blocks (the plan uses the same rule).
-template <typename T, int NKB>
-constexpr int rt_small() {
-    return (sizeof(T) == 4 && NKB <= EXEMCL_RT1_NKB32) ? 1 : 2;
+constexpr int plan_waves(int elem_bytes, int tile, int nkb) {
+    if (nkb <= EXEMCL_BIG_NKB) return EXEMCL_SMALL_WAVES;
+    return (elem_bytes == 2 && tile == 32 && nkb > 16) ? EXEMCL_WAVES16_BIG : EXEMCL_BIG_WAVES;
+}
+
+template <typename T, int TILE, int NKB>
+constexpr int rt_of() {
+    return plan_rt((int)sizeof(T), TILE, NKB);
+}
+
+template <typename T, int TILE, int NKB>
+constexpr int waves_of() {
+    return plan_waves((int)sizeof(T), TILE, NKB);
 }
 
 // One storage type: pick the instantiation for the plan's k-block bucket.
 template <typename T, int TILE, int MODE>
 hipError_t eval_dispatch(const MfmaPlan &pl, const MfmaArgs &x, hipStream_t st) {
-    if constexpr (TILE == 16) {
+    if constexpr (TILE == 16 && sizeof(T) == 4) {
         switch (pl.nkb) {
-        case 20: return eval_launch<T, TILE, 20, 4, 1, waves_for<20>(), MODE>(x, st);
-        case 24: return eval_launch<T, TILE, 24, 4, 1, waves_for<24>(), MODE>(x, st);
-        case 28: return eval_launch<T, TILE, 28, 4, 1, waves_for<28>(), MODE>(x, st);
-        case 32: return eval_launch<T, TILE, 32, 4, 1, waves_for<32>(), MODE>(x, st);
+        case 20: return eval_launch<T, TILE, 20, 4, rt_of<T, TILE, 20>(), waves_of<T, TILE, 20>(), MODE>(x, st);
+        case 24: return eval_launch<T, TILE, 24, 4, rt_of<T, TILE, 24>(), waves_of<T, TILE, 24>(), MODE>(x, st);
+        case 28: return eval_launch<T, TILE, 28, 4, rt_of<T, TILE, 28>(), waves_of<T, TILE, 28>(), MODE>(x, st);
+        case 32: return eval_launch<T, TILE, 32, 4, rt_of<T, TILE, 32>(), waves_of<T, TILE, 32>(), MODE>(x, st);
         }
     } else {
         constexpr int KL = Mfma<T, TILE>::KS_PER_KB;
         if (pl.nkb == 1) {
             if constexpr (KL == 4) {
                 switch (pl.nks_last) {
-                case 1: return eval_launch<T, TILE, 1, 1, rt_small<T, 1>(), waves_for<1>(), MODE>(x, st);
-                case 2: return eval_launch<T, TILE, 1, 2, rt_small<T, 1>(), waves_for<1>(), MODE>(x, st);
-                case 3: return eval_launch<T, TILE, 1, 3, rt_small<T, 1>(), waves_for<1>(), MODE>(x, st);
-                case 4: return eval_launch<T, TILE, 1, 4, rt_small<T, 1>(), waves_for<1>(), MODE>(x, st);
+                case 1: return eval_launch<T, TILE, 1, 1, rt_of<T, TILE, 1>(), waves_of<T, TILE, 1>(), MODE>(x, st);
+                case 2: return eval_launch<T, TILE, 1, 2, rt_of<T, TILE, 1>(), waves_of<T, TILE, 1>(), MODE>(x, st);
+                case 3: return eval_launch<T, TILE, 1, 3, rt_of<T, TILE, 1>(), waves_of<T, TILE, 1>(), MODE>(x, st);
+                case 4: return eval_launch<T, TILE, 1, 4, rt_of<T, TILE, 1>(), waves_of<T, TILE, 1>(), MODE>(x, st);
                 }
                 return hipErrorInvalidValue;
             } else {
-                return eval_launch<T, TILE, 1, KL, rt_small<T, 1>(), waves_for<1>(), MODE>(x, st);
+                return eval_launch<T, TILE, 1, KL, rt_of<T, TILE, 1>(), waves_of<T, TILE, 1>(), MODE>(x, st);
             }
         }
         switch (pl.nkb) {
-        case 2: return eval_launch<T, TILE, 2, KL, rt_small<T, 2>(), waves_for<2>(), MODE>(x, st);
-        case 3: return eval_launch<T, TILE, 3, KL, rt_small<T, 3>(), waves_for<3>(), MODE>(x, st);
-        case 4: return eval_launch<T, TILE, 4, KL, rt_small<T, 4>(), waves_for<4>(), MODE>(x, st);
-        case 5: return eval_launch<T, TILE, 5, KL, rt_small<T, 5>(), waves_for<5>(), MODE>(x, st);
-        case 6: return eval_launch<T, TILE, 6, KL, rt_small<T, 6>(), waves_for<6>(), MODE>(x, st);
-        case 7: return eval_launch<T, TILE, 7, KL, rt_small<T, 7>(), waves_for<7>(), MODE>(x, st);
-        case 8: return eval_launch<T, TILE, 8, KL, rt_small<T, 8>(), waves_for<8>(), MODE>(x, st);
-        case 10: return eval_launch<T, TILE, 10, KL, rt_small<T, 10>(), waves_for<10>(), MODE>(x, st);
-        case 12: return eval_launch<T, TILE, 12, KL, rt_small<T, 12>(), waves_for<12>(), MODE>(x, st);
-        case 13: return eval_launch<T, TILE, 13, KL, rt_small<T, 13>(), waves_for<13>(), MODE>(x, st);
-        case 14: return eval_launch<T, TILE, 14, KL, rt_small<T, 14>(), waves_for<14>(), MODE>(x, st);
-        case 16: return eval_launch<T, TILE, 16, KL, rt_small<T, 16>(), waves_for<16>(), MODE>(x, st);
-        case 20: return eval_launch<T, TILE, 20, KL, 1, waves_for<20>(), MODE>(x, st);
-        case 24: return eval_launch<T, TILE, 24, KL, 1, waves_for<24>(), MODE>(x, st);
-        case 28: return eval_launch<T, TILE, 28, KL, 1, waves_for<28>(), MODE>(x, st);
-        case 32: return eval_launch<T, TILE, 32, KL, 1, waves_for<32>(), MODE>(x, st);
+        case 2: return eval_launch<T, TILE, 2, KL, rt_of<T, TILE, 2>(), waves_of<T, TILE, 2>(), MODE>(x, st);
+        case 3: return eval_launch<T, TILE, 3, KL, rt_of<T, TILE, 3>(), waves_of<T, TILE, 3>(), MODE>(x, st);
+        case 4: return eval_launch<T, TILE, 4, KL, rt_of<T, TILE, 4>(), waves_of<T, TILE, 4>(), MODE>(x, st);
+        case 5: return eval_launch<T, TILE, 5, KL, rt_of<T, TILE, 5>(), waves_of<T, TILE, 5>(), MODE>(x, st);
+        case 6: return eval_launch<T, TILE, 6, KL, rt_of<T, TILE, 6>(), waves_of<T, TILE, 6>(), MODE>(x, st);
+        case 7: return eval_launch<T, TILE, 7, KL, rt_of<T, TILE, 7>(), waves_of<T, TILE, 7>(), MODE>(x, st);
+        case 8: return eval_launch<T, TILE, 8, KL, rt_of<T, TILE, 8>(), waves_of<T, TILE, 8>(), MODE>(x, st);
+        case 10: return eval_launch<T, TILE, 10, KL, rt_of<T, TILE, 10>(), waves_of<T, TILE, 10>(), MODE>(x, st);
+        case 12: return eval_launch<T, TILE, 12, KL, rt_of<T, TILE, 12>(), waves_of<T, TILE, 12>(), MODE>(x, st);
+        case 13: return eval_launch<T, TILE, 13, KL, rt_of<T, TILE, 13>(), waves_of<T, TILE, 13>(), MODE>(x, st);
+        case 14: return eval_launch<T, TILE, 14, KL, rt_of<T, TILE, 14>(), waves_of<T, TILE, 14>(), MODE>(x, st);
+        case 16: return eval_launch<T, TILE, 16, KL, rt_of<T, TILE, 16>(), waves_of<T, TILE, 16>(), MODE>(x, st);
+        }
+        // 16 k-blocks of 32 coordinates already cover d = 512 for the
+        // 16x16x32 shape; the 16- and 8-coordinate shapes need more.
+        if constexpr (Mfma<T, TILE>::KB_DIMS < 32) {
+            switch (pl.nkb) {
+            case 20: return eval_launch<T, TILE, 20, KL, rt_of<T, TILE, 20>(), waves_of<T, TILE, 20>(), MODE>(x, st);
+            case 24: return eval_launch<T, TILE, 24, KL, rt_of<T, TILE, 24>(), waves_of<T, TILE, 24>(), MODE>(x, st);
+            case 28: return eval_launch<T, TILE, 28, KL, rt_of<T, TILE, 28>(), waves_of<T, TILE, 28>(), MODE>(x, st);
+            case 32: return eval_launch<T, TILE, 32, KL, rt_of<T, TILE, 32>(), waves_of<T, TILE, 32>(), MODE>(x, st);
+            }
         }
     }
     return hipErrorInvalidValue;
