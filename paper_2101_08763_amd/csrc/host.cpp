@@ -40,6 +40,17 @@ int64_t workspace_limit() {
     return (end && *end == '\0' && v >= 0) ? (int64_t)v : INT64_MAX;
 }
 
+// Workgroups an MFMA launch aims for (EXEMCL_WG_TARGET overrides, for tuning):
+// enough to cover 256 CUs several times; a chunk of set groups shares one
+// load of a workgroup's points.
+int64_t wg_target() {
+    const char *s = getenv("EXEMCL_WG_TARGET");
+    if (!s || !*s) return 2048;
+    char *end = nullptr;
+    long long v = strtoll(s, &end, 10);
+    return (end && *end == '\0' && v >= 1 && v <= (1 << 24)) ? (int64_t)v : 2048;
+}
+
 // Path choice: a function of (d, k, precision) only.
 int choose_path(int64_t d, int64_t k, int precision) {
     MfmaPlan mp;
@@ -74,9 +85,8 @@ bool layout_eval(int64_t n, int64_t d, int64_t l, int64_t k, int precision, int 
         L->lpad = L->ngroups * tm;
         const int64_t nrb = (n + L->mp.rows - 1) / L->mp.rows;
         L->G = nrb * L->mp.waves;  // one partial-sum row per wavefront
-        // Enough workgroups to cover 256 CUs several times; a chunk of set
-        // groups shares one load of the workgroup's points.
-        int64_t chunks = (2048 + nrb - 1) / nrb;
+        const int64_t target = wg_target();
+        int64_t chunks = (target + nrb - 1) / nrb;
         if (chunks < 1) chunks = 1;
         if (chunks > L->ngroups) chunks = L->ngroups;
         if (chunks > 65535) chunks = 65535;

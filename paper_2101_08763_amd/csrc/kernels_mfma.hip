@@ -6,9 +6,15 @@
 #include "internal.h"
 #include "mfma_kernels.hpp"
 
-// fp16/bf16 rows of at least this many coordinates use the 16x16x32 shape.
+// fp16/bf16 rows of at least EXEMCL_F16_WIDE_D coordinates use the 16x16x32
+// shape, unless padding d to 32-coordinate k-blocks costs more than
+// EXEMCL_F16_WIDE_PAD percent over 16-coordinate ones (d = 100 pads to 128
+// instead of 112: the 32x32x16 shape is faster there).
 #ifndef EXEMCL_F16_WIDE_D
 #define EXEMCL_F16_WIDE_D 17
+#endif
+#ifndef EXEMCL_F16_WIDE_PAD
+#define EXEMCL_F16_WIDE_PAD 8
 #endif
 
 namespace exemcl {
@@ -39,7 +45,7 @@ bool mfma_plan(int prec, int64_t d, MfmaPlan *p) {
         q.kb_dims = 16;
         q.nkb = bucket((int)((d + 15) / 16));
         q.nks_last = 4;
-    } else if (d >= EXEMCL_F16_WIDE_D) {
+    } else if (d >= EXEMCL_F16_WIDE_D && (d + 31) / 32 * 32 * 100 <= (d + 15) / 16 * 16 * (100 + EXEMCL_F16_WIDE_PAD)) {
         // v_mfma_f32_16x16x32_{f16,bf16}, 32 coordinates per k-block, two
         // set members per tile
         q.tile = 16;
@@ -64,7 +70,7 @@ bool mfma_plan(int prec, int64_t d, MfmaPlan *p) {
     return true;
 }
 
-int64_t mfma_tile_bytes(const MfmaPlan &pl) { return HDR + (int64_t)pl.nkb * pl.nb * 1024; }
+int64_t mfma_tile_bytes(const MfmaPlan &pl) { return hdr_bytes(pl.tile, pl.nb) + (int64_t)pl.nkb * pl.nb * 1024; }
 
 int64_t mfma_tiles_per_group(const MfmaPlan &pl, int64_t k) { return (k + pl.nb - 1) / pl.nb; }
 

@@ -36,11 +36,13 @@
 
 namespace exemcl {
 
-constexpr int HDR = 128;  // tile header: TM * NB fp32 biases, padded to 128 bytes
+// Tile header: the TM * NB fp32 biases of a tile's columns, padded to a
+// multiple of 128 bytes.
+constexpr int hdr_bytes(int tm, int nb) { return (tm * nb * 4 + 127) / 128 * 128; }
 
-template <int NKB>
+template <int NF, int HDRB>
 constexpr int tile_bytes_of() {
-    return HDR + NKB * 1024;
+    return HDRB + NF * 1024;
 }
 
 // ---------------------------------------------------------------------------
@@ -72,6 +74,7 @@ __global__ __launch_bounds__(64) void pack_tiles_kernel(const T *__restrict__ V,
     const int lane = threadIdx.x;
     const int col = lane % M::TM, grp = lane / M::TM;
     const int64_t j = g * M::TM + col;
+    constexpr int HDR = hdr_bytes(M::TM, NB);
     unsigned char *tile = tiles + t * (int64_t)(HDR + nkb * NB * 1024);
     typename M::vec_t *dst = reinterpret_cast<typename M::vec_t *>(tile + HDR);
 #pragma unroll
@@ -191,24 +194,24 @@ constexpr int lds_budget() {
     return WAVES <= 4 ? kLdsBytes / 2 : kLdsBytes;
 }
 
-template <int NKB, int WAVES>
+template <int NKB, int WAVES, int HDRB>
 constexpr int tiles_per_stage() {
-    constexpr int tb = tile_bytes_of<NKB>();
+    constexpr int tb = tile_bytes_of<NKB, HDRB>();
     int tps = NKB <= EXEMCL_BIG_NKB ? (EXEMCL_STAGE_MIN / tb > 1 ? EXEMCL_STAGE_MIN / tb : 1) : EXEMCL_TPS_BIG;
     while (tps > 1 && 2 * round_stage<NKB, WAVES>(tps * tb) > lds_budget<WAVES>()) --tps;
     return tps;
 }
 
-template <int NKB, int WAVES>
+template <int NKB, int WAVES, int HDRB>
 constexpr int stage_bytes() {
-    return round_stage<NKB, WAVES>(tiles_per_stage<NKB, WAVES>() * tile_bytes_of<NKB>());
+    return round_stage<NKB, WAVES>(tiles_per_stage<NKB, WAVES, HDRB>() * tile_bytes_of<NKB, HDRB>());
 }
 
-template <int NKB, int WAVES>
+template <int NKB, int WAVES, int HDRB>
 constexpr int ring_depth() {
     constexpr int want = NKB <= EXEMCL_BIG_NKB ? EXEMCL_RING_SMALL : EXEMCL_RING_BIG;
-    constexpr int fit = (stage_bytes<NKB, WAVES>() * 2 <= lds_budget<WAVES>() ? lds_budget<WAVES>() : kLdsBytes) /
-                        stage_bytes<NKB, WAVES>();
+    constexpr int sb = stage_bytes<NKB, WAVES, HDRB>();
+    constexpr int fit = (sb * 2 <= lds_budget<WAVES>() ? lds_budget<WAVES>() : kLdsBytes) / sb;
     return want < fit ? want : fit;
 }
 
@@ -265,11 +268,12 @@ __global__ __launch_bounds__(WAVES * 64) void eval_mfma_kernel(const T *__restri
     constexpr int NB = M::NB;     // column groups (set members) per tile
     constexpr int NF = NKB * NB;  // B fragments per tile, fragment f = kb * NB + h
     constexpr int NT = WAVES * 64;
-    constexpr int TB = tile_bytes_of<NF>();
-    constexpr int SB = stage_bytes<NF, WAVES>();
-    constexpr int TPS = tiles_per_stage<NF, WAVES>();
+    constexpr int HDR = hdr_bytes(TM, NB);
+    constexpr int TB = tile_bytes_of<NF, HDR>();
+    constexpr int SB = stage_bytes<NF, WAVES, HDR>();
+    constexpr int TPS = tiles_per_stage<NF, WAVES, HDR>();
     constexpr int CNT = SB / (NT * 16);
-    constexpr int NBUF = ring_depth<NF, WAVES>();
+    constexpr int NBUF = ring_depth<NF, WAVES, HDR>();
     // Reads across tiles pay off for long tiles; short ones keep the registers
     // for a third wavefront per SIMD instead.
     constexpr bool SCHED = (sizeof(T) == 4 ? EXEMCL_SCHED32 : EXEMCL_SCHED16) && NF >= EXEMCL_SCHED_MIN_NF;
@@ -278,7 +282,6 @@ __global__ __launch_bounds__(WAVES * 64) void eval_mfma_kernel(const T *__restri
     // divides NF; the next tile then finds fragment i in slot i.
     constexpr int PF = SCHED ? prefetch_depth(NF, EXEMCL_PF_SCHED) : (NF < EXEMCL_PF ? NF : EXEMCL_PF);
     static_assert(!SCHED || NF % PF == 0, "cross-tile prefetch ring must wrap at the tile end");
-    static_assert(TM * NB * 4 <= HDR, "tile header holds every column's bias");
     static_assert(MODE == MODE_SUM || NB == 1, "the row-max mode stages one member per tile");
     constexpr bool PAIR = EXEMCL_PAIR && NB == 1 && NKB <= (sizeof(T) == 4 ? EXEMCL_PAIR_NKB32 : EXEMCL_PAIR_NKB16);
     static_assert(TPS >= 1 && TPS * TB <= SB && NBUF >= 2 && NBUF * SB <= kLdsBytes, "stage geometry");
@@ -582,8 +585,9 @@ hipError_t pack_launch(const MfmaPlan &pl, const void *V, int64_t n, int ld, con
 template <typename T, int TILE, int NKB, int NKS_LAST, int RT, int WAVES, int MODE, bool HAS_M0>
 hipError_t eval_launch_t(const MfmaArgs &x, hipStream_t st) {
     constexpr int NF = NKB * Mfma<T, TILE>::NB;
-    constexpr int SB = stage_bytes<NF, WAVES>();
-    constexpr int NBUF = ring_depth<NF, WAVES>();
+    constexpr int HDRB = hdr_bytes(TILE, Mfma<T, TILE>::NB);
+    constexpr int SB = stage_bytes<NF, WAVES, HDRB>();
+    constexpr int NBUF = ring_depth<NF, WAVES, HDRB>();
     auto kern = eval_mfma_kernel<T, TILE, NKB, NKS_LAST, RT, WAVES, MODE, HAS_M0>;
     const size_t lds = (size_t)NBUF * SB;
     if (lds > 64 * 1024) {
