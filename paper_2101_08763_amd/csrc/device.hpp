@@ -16,6 +16,9 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 // Element conversion to fp32 (exact for all three storage types).
@@ -59,6 +62,8 @@ struct Mfma<float, 32> {
     using acc_t = f32x16;
     using vec_t = f32x4;
     using elem_t = float;
+    static constexpr bool HAS_HALF = false;  // no half k-block
+    using hvec_t = vec_t;
     __device__ __forceinline__ static int dim(int kb, int grp, int e) { return kb * KB_DIMS + grp * VEC + e; }
     __device__ __forceinline__ static acc_t mma(vec_t a, vec_t b, int e, acc_t c) {
         return __builtin_amdgcn_mfma_f32_32x32x2f32(a[e], b[e], c, 0, 0, 0);
@@ -75,6 +80,8 @@ struct Mfma<float, 16> {
     using acc_t = f32x4;
     using vec_t = f32x4;
     using elem_t = float;
+    static constexpr bool HAS_HALF = false;  // no half k-block
+    using hvec_t = vec_t;
     __device__ __forceinline__ static int dim(int kb, int grp, int e) { return kb * KB_DIMS + grp * VEC + e; }
     __device__ __forceinline__ static acc_t mma(vec_t a, vec_t b, int e, acc_t c) {
         return __builtin_amdgcn_mfma_f32_16x16x4f32(a[e], b[e], c, 0, 0, 0);
@@ -90,6 +97,8 @@ struct Mfma<_Float16, 32> {
     using acc_t = f32x16;
     using vec_t = f16x8;
     using elem_t = _Float16;
+    static constexpr bool HAS_HALF = false;  // no half k-block
+    using hvec_t = vec_t;
     __device__ __forceinline__ static int dim(int kb, int grp, int e) { return kb * KB_DIMS + grp * VEC + e; }
     __device__ __forceinline__ static acc_t mma(vec_t a, vec_t b, int, acc_t c) {
         return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
@@ -104,6 +113,8 @@ struct Mfma<__bf16, 32> {
     using acc_t = f32x16;
     using vec_t = bf16x8;
     using elem_t = __bf16;
+    static constexpr bool HAS_HALF = false;  // no half k-block
+    using hvec_t = vec_t;
     __device__ __forceinline__ static int dim(int kb, int grp, int e) { return kb * KB_DIMS + grp * VEC + e; }
     __device__ __forceinline__ static acc_t mma(vec_t a, vec_t b, int, acc_t c) {
         return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
@@ -129,6 +140,15 @@ struct Mfma<_Float16, 16> {
     __device__ __forceinline__ static acc_t mma(vec_t a, vec_t b, int, acc_t c) {
         return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
     }
+    // Half k-block (16 coordinates, v_mfma_f32_16x16x16_f16): lane L holds
+    // coordinates kb*32 + (L/16)*4 + {0..3} as an 8-byte vector.
+    static constexpr bool HAS_HALF = true;
+    static constexpr int HVEC = 4;
+    using hvec_t = f16x4;
+    __device__ __forceinline__ static int hdim(int kb, int grp, int e) { return kb * KB_DIMS + grp * HVEC + e; }
+    __device__ __forceinline__ static acc_t mma_half(hvec_t a, hvec_t b, acc_t c) {
+        return __builtin_amdgcn_mfma_f32_16x16x16f16(a, b, c, 0, 0, 0);
+    }
 };
 
 // bf16: v_mfma_f32_16x16x32_bf16 (gfx950), same layout as fp16.
@@ -142,6 +162,15 @@ struct Mfma<__bf16, 16> {
     __device__ __forceinline__ static int dim(int kb, int grp, int e) { return kb * KB_DIMS + grp * VEC + e; }
     __device__ __forceinline__ static acc_t mma(vec_t a, vec_t b, int, acc_t c) {
         return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+    }
+    // Half k-block (v_mfma_f32_16x16x16_bf16), same layout as fp16.
+    static constexpr bool HAS_HALF = true;
+    static constexpr int HVEC = 4;
+    using hvec_t = bf16x4;
+    __device__ __forceinline__ static int hdim(int kb, int grp, int e) { return kb * KB_DIMS + grp * HVEC + e; }
+    __device__ __forceinline__ static acc_t mma_half(hvec_t a, hvec_t b, acc_t c) {
+        return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(i16x4, a), __builtin_bit_cast(i16x4, b), c, 0,
+                                                         0, 0);
     }
 };
 
@@ -192,6 +221,11 @@ constexpr uint32_t kDeadOffset = 0x80000000u;
 template <typename vec_t>
 __device__ __forceinline__ vec_t window_load16(__amdgpu_buffer_rsrc_t rsrc, uint32_t off) {
     return __builtin_bit_cast(vec_t, __builtin_amdgcn_raw_buffer_load_b128(rsrc, (int)off, 0, 0));
+}
+
+template <typename hvec_t>
+__device__ __forceinline__ hvec_t window_load8(__amdgpu_buffer_rsrc_t rsrc, uint32_t off) {
+    return __builtin_bit_cast(hvec_t, __builtin_amdgcn_raw_buffer_load_b64(rsrc, (int)off, 0, 0));
 }
 
 __device__ __forceinline__ float window_load4(__amdgpu_buffer_rsrc_t rsrc, uint32_t off) {

@@ -24,6 +24,7 @@ struct MfmaPlan {
     int rows;       // rows per workgroup = waves * rt * tile
     int kb_dims;    // coordinates per k-block
     int nb;         // set members per staged tile (a set group spans ceil(k / nb) tiles)
+    int half;       // 1: the last k-block holds 16 coordinates (16x16x16 instruction)
 };
 
 bool mfma_plan(int prec, int64_t d, MfmaPlan *p);

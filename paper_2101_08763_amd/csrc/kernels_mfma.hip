@@ -7,14 +7,18 @@
 #include "mfma_kernels.hpp"
 
 // fp16/bf16 rows of at least EXEMCL_F16_WIDE_D coordinates use the 16x16x32
-// shape, unless padding d to 32-coordinate k-blocks costs more than
-// EXEMCL_F16_WIDE_PAD percent over 16-coordinate ones (d = 100 pads to 128
-// instead of 112: the 32x32x16 shape is faster there).
+// shape.  Up to EXEMCL_HALF_MAX_D coordinates a last k-block of 16 covers
+// d mod 32 in (0, 16] (d = 100: 3 x 32 + 16 = 112 instead of 128); above it
+// d pads to whole 32-coordinate blocks (at most 8 % more work) and long tiles
+// keep their cross-tile prefetch, which a half block does not take part in.
 #ifndef EXEMCL_F16_WIDE_D
 #define EXEMCL_F16_WIDE_D 17
 #endif
-#ifndef EXEMCL_F16_WIDE_PAD
-#define EXEMCL_F16_WIDE_PAD 8
+#ifndef EXEMCL_HALF_MAX_D
+#define EXEMCL_HALF_MAX_D 192
+#endif
+#if EXEMCL_HALF_MAX_D > 192
+#error "half k-blocks are compiled for 2 to 6 k-blocks (d <= 192)"
 #endif
 
 namespace exemcl {
@@ -33,6 +37,7 @@ bool mfma_plan(int prec, int64_t d, MfmaPlan *p) {
     MfmaPlan q{};
     q.waves = 4;
     q.nb = 1;
+    q.half = 0;
     if (prec == P_FP32 && d <= 256) {
         // v_mfma_f32_32x32x2_f32, 8 coordinates per k-block
         q.tile = 32;
@@ -45,14 +50,16 @@ bool mfma_plan(int prec, int64_t d, MfmaPlan *p) {
         q.kb_dims = 16;
         q.nkb = bucket((int)((d + 15) / 16));
         q.nks_last = 4;
-    } else if (d >= EXEMCL_F16_WIDE_D && (d + 31) / 32 * 32 * 100 <= (d + 15) / 16 * 16 * (100 + EXEMCL_F16_WIDE_PAD)) {
+    } else if (d >= EXEMCL_F16_WIDE_D) {
         // v_mfma_f32_16x16x32_{f16,bf16}, 32 coordinates per k-block, two
-        // set members per tile
+        // set members per tile; when d mod 32 is in (0, 16] the last k-block
+        // holds 16 coordinates (v_mfma_f32_16x16x16) instead of padding to 32
         q.tile = 16;
         q.kb_dims = 32;
         q.nkb = bucket((int)((d + 31) / 32));
         q.nks_last = 1;
         q.nb = EXEMCL_NB16;
+        q.half = (d % 32 != 0 && d % 32 <= 16 && d <= EXEMCL_HALF_MAX_D && q.nkb == (d + 31) / 32) ? 1 : 0;
     } else {
         // v_mfma_f32_32x32x16_{f16,bf16}, 16 coordinates per k-block (one
         // k-block for d <= 16, where 32-coordinate blocks would be half padding)
@@ -70,7 +77,9 @@ bool mfma_plan(int prec, int64_t d, MfmaPlan *p) {
     return true;
 }
 
-int64_t mfma_tile_bytes(const MfmaPlan &pl) { return hdr_bytes(pl.tile, pl.nb) + (int64_t)pl.nkb * pl.nb * 1024; }
+int64_t mfma_tile_bytes(const MfmaPlan &pl) {
+    return hdr_bytes(pl.tile, pl.nb) + (int64_t)(pl.nkb - pl.half) * pl.nb * 1024 + (int64_t)pl.half * pl.nb * 512;
+}
 
 int64_t mfma_tiles_per_group(const MfmaPlan &pl, int64_t k) { return (k + pl.nb - 1) / pl.nb; }
 

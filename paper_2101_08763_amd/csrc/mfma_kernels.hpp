@@ -40,10 +40,9 @@ namespace exemcl {
 // multiple of 128 bytes.
 constexpr int hdr_bytes(int tm, int nb) { return (tm * nb * 4 + 127) / 128 * 128; }
 
-template <int NF, int HDRB>
-constexpr int tile_bytes_of() {
-    return HDRB + NF * 1024;
-}
+// Bytes of a staged tile: header, NFF whole fragments of 1 KiB and, when the
+// last k-block is a half one, NB half fragments of 512 bytes.
+constexpr int tile_bytes_of(int hdr, int nff, int nhalf) { return hdr + nff * 1024 + nhalf * 512; }
 
 // ---------------------------------------------------------------------------
 // Staging: gather exemplar rows by index into tiles, with their norms.
@@ -65,7 +64,8 @@ constexpr int tile_bytes_of() {
 template <typename T, int TILE>
 __global__ __launch_bounds__(64) void pack_tiles_kernel(const T *__restrict__ V, int64_t n, int ld,
                                                         const int32_t *__restrict__ sets, int64_t l,
-                                                        int64_t k, int nkb, unsigned char *__restrict__ tiles) {
+                                                        int64_t k, int nkb, int half,
+                                                        unsigned char *__restrict__ tiles) {
     using M = Mfma<T, TILE>;
     constexpr int NB = M::NB;
     const int64_t kt = (k + NB - 1) / NB;
@@ -75,7 +75,8 @@ __global__ __launch_bounds__(64) void pack_tiles_kernel(const T *__restrict__ V,
     const int col = lane % M::TM, grp = lane / M::TM;
     const int64_t j = g * M::TM + col;
     constexpr int HDR = hdr_bytes(M::TM, NB);
-    unsigned char *tile = tiles + t * (int64_t)(HDR + nkb * NB * 1024);
+    const int nfull = nkb - half;  // whole k-blocks; a half one follows when half = 1
+    unsigned char *tile = tiles + t * (int64_t)tile_bytes_of(HDR, nfull * NB, half * NB);
     typename M::vec_t *dst = reinterpret_cast<typename M::vec_t *>(tile + HDR);
 #pragma unroll
     for (int h = 0; h < NB; ++h) {
@@ -85,7 +86,7 @@ __global__ __launch_bounds__(64) void pack_tiles_kernel(const T *__restrict__ V,
         const bool valid = idx >= 0 && idx < n;
         const int64_t r = valid ? idx : n;  // row n reads as zeros
         float sq = 0.0f;
-        for (int kb = 0; kb < nkb; ++kb) {
+        for (int kb = 0; kb < nfull; ++kb) {
             const typename M::vec_t v =
                 lanevec_keep<M>(lanevec_raw<M>(V, n, ld, r, kb, grp), lanevec_live<M>(n, ld, r, kb, grp));
             dst[(kb * NB + h) * 64 + lane] = v;
@@ -93,6 +94,24 @@ __global__ __launch_bounds__(64) void pack_tiles_kernel(const T *__restrict__ V,
             for (int e = 0; e < M::VEC; ++e) {
                 const float x = to_f32(v[e]);
                 sq = fmaf(x, x, sq);
+            }
+        }
+        if constexpr (M::HAS_HALF) {
+            if (half) {
+                // Half fragment h: lane L's 8 bytes = coordinates
+                // nfull*32 + (L/TM)*4 + {0..3}, after all whole fragments.
+                using hvec_t = typename M::hvec_t;
+                const int d0 = M::hdim(nfull, grp, 0);
+                const bool live = r < n && d0 < ld;  // ld and d0 are multiples of 4: all 4 in the row
+                hvec_t v = *reinterpret_cast<const hvec_t *>(V + (live ? r : 0) * (int64_t)ld + (live ? d0 : 0));
+#pragma unroll
+                for (int e = 0; e < M::HVEC; ++e) v[e] = live ? v[e] : (typename M::elem_t)0.0f;
+                reinterpret_cast<hvec_t *>(tile + HDR + nfull * NB * 1024)[h * 64 + lane] = v;
+#pragma unroll
+                for (int e = 0; e < M::HVEC; ++e) {
+                    const float x = to_f32(v[e]);
+                    sq = fmaf(x, x, sq);
+                }
             }
         }
 #pragma unroll
@@ -194,23 +213,23 @@ constexpr int lds_budget() {
     return WAVES <= 4 ? kLdsBytes / 2 : kLdsBytes;
 }
 
-template <int NKB, int WAVES, int HDRB>
+// Stage geometry for tiles of TB bytes and NFRAG B fragments.
+template <int TB, int NFRAG, int WAVES>
 constexpr int tiles_per_stage() {
-    constexpr int tb = tile_bytes_of<NKB, HDRB>();
-    int tps = NKB <= EXEMCL_BIG_NKB ? (EXEMCL_STAGE_MIN / tb > 1 ? EXEMCL_STAGE_MIN / tb : 1) : EXEMCL_TPS_BIG;
-    while (tps > 1 && 2 * round_stage<NKB, WAVES>(tps * tb) > lds_budget<WAVES>()) --tps;
+    int tps = NFRAG <= EXEMCL_BIG_NKB ? (EXEMCL_STAGE_MIN / TB > 1 ? EXEMCL_STAGE_MIN / TB : 1) : EXEMCL_TPS_BIG;
+    while (tps > 1 && 2 * round_stage<NFRAG, WAVES>(tps * TB) > lds_budget<WAVES>()) --tps;
     return tps;
 }
 
-template <int NKB, int WAVES, int HDRB>
+template <int TB, int NFRAG, int WAVES>
 constexpr int stage_bytes() {
-    return round_stage<NKB, WAVES>(tiles_per_stage<NKB, WAVES, HDRB>() * tile_bytes_of<NKB, HDRB>());
+    return round_stage<NFRAG, WAVES>(tiles_per_stage<TB, NFRAG, WAVES>() * TB);
 }
 
-template <int NKB, int WAVES, int HDRB>
+template <int TB, int NFRAG, int WAVES>
 constexpr int ring_depth() {
-    constexpr int want = NKB <= EXEMCL_BIG_NKB ? EXEMCL_RING_SMALL : EXEMCL_RING_BIG;
-    constexpr int sb = stage_bytes<NKB, WAVES, HDRB>();
+    constexpr int want = NFRAG <= EXEMCL_BIG_NKB ? EXEMCL_RING_SMALL : EXEMCL_RING_BIG;
+    constexpr int sb = stage_bytes<TB, NFRAG, WAVES>();
     constexpr int fit = (sb * 2 <= lds_budget<WAVES>() ? lds_budget<WAVES>() : kLdsBytes) / sb;
     return want < fit ? want : fit;
 }
@@ -254,7 +273,7 @@ __device__ __forceinline__ void wait_vmcnt() {
 // MODE_ROWMAX: rowmax[v] = max(m0(v), 0, max over all staged columns of
 // h_s(v)) (m0 = 0 when null); rowmax must not alias m0.
 // ---------------------------------------------------------------------------
-template <typename T, int TILE, int NKB, int NKS_LAST, int RT, int WAVES, int MODE, bool HAS_M0>
+template <typename T, int TILE, int NKB, int NKS_LAST, int RT, int WAVES, int MODE, bool HAS_M0, bool HALF>
 __global__ __launch_bounds__(WAVES * 64) void eval_mfma_kernel(const T *__restrict__ V, int64_t n, int ld,
                                                                  const unsigned char *__restrict__ tiles, int64_t kt,
                                                                  int64_t ngroups, int64_t gpc,
@@ -267,20 +286,24 @@ __global__ __launch_bounds__(WAVES * 64) void eval_mfma_kernel(const T *__restri
     constexpr int TM = M::TM;
     constexpr int NB = M::NB;     // column groups (set members) per tile
     constexpr int NF = NKB * NB;  // B fragments per tile, fragment f = kb * NB + h
+    // With HALF the last k-block holds 16 coordinates: its NB half fragments
+    // (512 bytes each) follow the NFF whole ones and bypass the prefetch ring.
+    constexpr int NFF = HALF ? (NKB - 1) * NB : NF;
     constexpr int NT = WAVES * 64;
     constexpr int HDR = hdr_bytes(TM, NB);
-    constexpr int TB = tile_bytes_of<NF, HDR>();
-    constexpr int SB = stage_bytes<NF, WAVES, HDR>();
-    constexpr int TPS = tiles_per_stage<NF, WAVES, HDR>();
+    constexpr int TB = tile_bytes_of(HDR, NFF, HALF ? NB : 0);
+    constexpr int SB = stage_bytes<TB, NF, WAVES>();
+    constexpr int TPS = tiles_per_stage<TB, NF, WAVES>();
     constexpr int CNT = SB / (NT * 16);
-    constexpr int NBUF = ring_depth<NF, WAVES, HDR>();
+    constexpr int NBUF = ring_depth<TB, NF, WAVES>();
+    static_assert(!HALF || (M::HAS_HALF && NKB >= 2), "half k-block needs the 16x16x16 instruction and a whole block");
     // Reads across tiles pay off for long tiles; short ones keep the registers
     // for a third wavefront per SIMD instead.
-    constexpr bool SCHED = (sizeof(T) == 4 ? EXEMCL_SCHED32 : EXEMCL_SCHED16) && NF >= EXEMCL_SCHED_MIN_NF;
+    constexpr bool SCHED = (sizeof(T) == 4 ? EXEMCL_SCHED32 : EXEMCL_SCHED16) && NF >= EXEMCL_SCHED_MIN_NF && !HALF;
     // B fragments in flight ahead of use.  When the reads run across tiles
     // (SCHED) the ring of PF slots must wrap exactly at a tile's end, so PF
     // divides NF; the next tile then finds fragment i in slot i.
-    constexpr int PF = SCHED ? prefetch_depth(NF, EXEMCL_PF_SCHED) : (NF < EXEMCL_PF ? NF : EXEMCL_PF);
+    constexpr int PF = SCHED ? prefetch_depth(NF, EXEMCL_PF_SCHED) : (NFF < EXEMCL_PF ? NFF : EXEMCL_PF);
     static_assert(!SCHED || NF % PF == 0, "cross-tile prefetch ring must wrap at the tile end");
     static_assert(MODE == MODE_SUM || NB == 1, "the row-max mode stages one member per tile");
     constexpr bool PAIR = EXEMCL_PAIR && NB == 1 && NKB <= (sizeof(T) == 4 ? EXEMCL_PAIR_NKB32 : EXEMCL_PAIR_NKB16);
@@ -324,7 +347,10 @@ __global__ __launch_bounds__(WAVES * 64) void eval_mfma_kernel(const T *__restri
 
     // Ground points of this wavefront, in A-operand order, resident for the
     // whole kernel (zero past d and past n).
-    vec_t a[RT][NKB];
+    constexpr int NKF = HALF ? NKB - 1 : NKB;  // whole k-blocks
+    using hvec_t = typename M::hvec_t;
+    vec_t a[RT][NKF];
+    hvec_t ah[HALF ? RT : 1];  // the half k-block's 8-byte lane vectors
     // The workgroup's rows as one buffer window (at most 512 rows of at most
     // 512 elements, so 32-bit offsets): rows past n read as zeros, and so do
     // vectors past ld, without a branch.
@@ -332,13 +358,18 @@ __global__ __launch_bounds__(WAVES * 64) void eval_mfma_kernel(const T *__restri
     const int64_t wrows = min((int64_t)(WAVES * RT * TM), n - wrow0);
     const auto vwin = window_rsrc(V + wrow0 * (int64_t)ld, (uint32_t)(wrows * ld * (int64_t)sizeof(T)));
 #pragma unroll
-    for (int rt = 0; rt < RT; ++rt)
+    for (int rt = 0; rt < RT; ++rt) {
+        const int lrow = wave * RT * TM + rt * TM + lr;
 #pragma unroll
-        for (int kb = 0; kb < NKB; ++kb) {
+        for (int kb = 0; kb < NKF; ++kb) {
             const int d0 = M::dim(kb, grp, 0);
-            const int lrow = wave * RT * TM + rt * TM + lr;
             a[rt][kb] = window_load16<vec_t>(vwin, d0 < ld ? (uint32_t)((lrow * ld + d0) * (int)sizeof(T)) : kDeadOffset);
         }
+        if constexpr (HALF) {
+            const int d0 = M::hdim(NKF, grp, 0);  // ld and d0 are multiples of 4: the 4 elements are in the row
+            ah[rt] = window_load8<hvec_t>(vwin, d0 < ld ? (uint32_t)((lrow * ld + d0) * (int)sizeof(T)) : kDeadOffset);
+        }
+    }
 
     // Initial value of the running max for each output element: e0's 0, or
     // (HAS_M0) the per-point cached value when scoring S u {c}.
@@ -396,14 +427,14 @@ __global__ __launch_bounds__(WAVES * 64) void eval_mfma_kernel(const T *__restri
 #pragma unroll
         for (int h = 0; h < NB; ++h) bias_next[h] = 0.0f;
 #pragma unroll
-        for (int kb = 0; kb < NKB; ++kb) {
+        for (int kb = 0; kb < NKF; ++kb) {
             vec_t bv[NB];
 #pragma unroll
             for (int h = 0; h < NB; ++h) {
                 const int f = kb * NB + h;
                 bv[h] = bq[f % PF];
                 const int ahead = f + PF;
-                if (ahead < NF) {
+                if (ahead < NFF) {
                     bq[f % PF] = B[ahead * 64 + lane];
                 } else if constexpr (SCHED) {
                     bq[f % PF] = Bn[(ahead - NF) * 64 + lane];
@@ -425,6 +456,16 @@ __global__ __launch_bounds__(WAVES * 64) void eval_mfma_kernel(const T *__restri
                 }
             }
             fence();
+        }
+        if constexpr (HALF) {
+            const hvec_t *Bh = reinterpret_cast<const hvec_t *>(tb + HDR + NFF * 1024);
+            hvec_t bh[NB];
+#pragma unroll
+            for (int h = 0; h < NB; ++h) bh[h] = Bh[h * 64 + lane];
+#pragma unroll
+            for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+                for (int h = 0; h < NB; ++h) acc[rt][h] = M::mma_half(ah[rt], bh[h], acc[rt][h]);
         }
         if constexpr (SCHED) {
 #pragma unroll
@@ -575,20 +616,22 @@ __global__ __launch_bounds__(WAVES * 64) void eval_mfma_kernel(const T *__restri
 template <typename T, int TILE>
 hipError_t pack_launch(const MfmaPlan &pl, const void *V, int64_t n, int ld, const int32_t *sets, int64_t l,
                        int64_t k, void *tiles, hipStream_t st) {
+    if (pl.half && !Mfma<T, TILE>::HAS_HALF) return hipErrorInvalidValue;
     const int64_t ngroups = (l + TILE - 1) / TILE;
     const int64_t kt = (k + Mfma<T, TILE>::NB - 1) / Mfma<T, TILE>::NB;
     hipLaunchKernelGGL((pack_tiles_kernel<T, TILE>), dim3((unsigned)(ngroups * kt)), dim3(64), 0, st,
-                       (const T *)V, n, ld, sets, l, k, pl.nkb, (unsigned char *)tiles);
+                       (const T *)V, n, ld, sets, l, k, pl.nkb, pl.half, (unsigned char *)tiles);
     return hipGetLastError();
 }
 
-template <typename T, int TILE, int NKB, int NKS_LAST, int RT, int WAVES, int MODE, bool HAS_M0>
+template <typename T, int TILE, int NKB, int NKS_LAST, int RT, int WAVES, int MODE, bool HAS_M0, bool HALF>
 hipError_t eval_launch_t(const MfmaArgs &x, hipStream_t st) {
-    constexpr int NF = NKB * Mfma<T, TILE>::NB;
-    constexpr int HDRB = hdr_bytes(TILE, Mfma<T, TILE>::NB);
-    constexpr int SB = stage_bytes<NF, WAVES, HDRB>();
-    constexpr int NBUF = ring_depth<NF, WAVES, HDRB>();
-    auto kern = eval_mfma_kernel<T, TILE, NKB, NKS_LAST, RT, WAVES, MODE, HAS_M0>;
+    constexpr int NB = Mfma<T, TILE>::NB;
+    constexpr int NF = NKB * NB;
+    constexpr int TB = tile_bytes_of(hdr_bytes(TILE, NB), HALF ? (NKB - 1) * NB : NF, HALF ? NB : 0);
+    constexpr int SB = stage_bytes<TB, NF, WAVES>();
+    constexpr int NBUF = ring_depth<TB, NF, WAVES>();
+    auto kern = eval_mfma_kernel<T, TILE, NKB, NKS_LAST, RT, WAVES, MODE, HAS_M0, HALF>;
     const size_t lds = (size_t)NBUF * SB;
     if (lds > 64 * 1024) {
         hipError_t e = hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
@@ -603,12 +646,12 @@ hipError_t eval_launch_t(const MfmaArgs &x, hipStream_t st) {
     return hipGetLastError();
 }
 
-template <typename T, int TILE, int NKB, int NKS_LAST, int RT, int WAVES, int MODE>
+template <typename T, int TILE, int NKB, int NKS_LAST, int RT, int WAVES, int MODE, bool HALF = false>
 hipError_t eval_launch(const MfmaArgs &x, hipStream_t st) {
     if constexpr (sizeof(T) == 4) {
-        if (x.m0) return eval_launch_t<T, TILE, NKB, NKS_LAST, RT, WAVES, MODE, true>(x, st);
+        if (x.m0) return eval_launch_t<T, TILE, NKB, NKS_LAST, RT, WAVES, MODE, true, HALF>(x, st);
     }
-    return eval_launch_t<T, TILE, NKB, NKS_LAST, RT, WAVES, MODE, false>(x, st);
+    return eval_launch_t<T, TILE, NKB, NKS_LAST, RT, WAVES, MODE, false, HALF>(x, st);
 }
 
 // Row tiles per wavefront and wavefronts per workgroup for a k-block bucket,
@@ -647,6 +690,20 @@ hipError_t eval_dispatch(const MfmaPlan &pl, const MfmaArgs &x, hipStream_t st) 
         }
     } else {
         constexpr int KL = Mfma<T, TILE>::KS_PER_KB;
+        if constexpr (Mfma<T, TILE>::HAS_HALF) {
+            if (pl.half) {
+                // d mod 32 in (0, 16] up to the plan's limit: 2 .. 6 k-blocks.
+                switch (pl.nkb) {
+                case 2: return eval_launch<T, TILE, 2, KL, rt_of<T, TILE, 2>(), waves_of<T, TILE, 2>(), MODE, true>(x, st);
+                case 3: return eval_launch<T, TILE, 3, KL, rt_of<T, TILE, 3>(), waves_of<T, TILE, 3>(), MODE, true>(x, st);
+                case 4: return eval_launch<T, TILE, 4, KL, rt_of<T, TILE, 4>(), waves_of<T, TILE, 4>(), MODE, true>(x, st);
+                case 5: return eval_launch<T, TILE, 5, KL, rt_of<T, TILE, 5>(), waves_of<T, TILE, 5>(), MODE, true>(x, st);
+                case 6: return eval_launch<T, TILE, 6, KL, rt_of<T, TILE, 6>(), waves_of<T, TILE, 6>(), MODE, true>(x, st);
+                }
+                return hipErrorInvalidValue;
+            }
+        }
+        if (pl.half) return hipErrorInvalidValue;
         if (pl.nkb == 1) {
             if constexpr (KL == 4) {
                 switch (pl.nks_last) {
