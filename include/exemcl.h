@@ -99,11 +99,53 @@ enum exemcl_path {
  * O(l*k*d) bytes) come from the library's pool; when the whole batch does not
  * fit (or exceeds EXEMCL_WORKSPACE_LIMIT bytes), the batch is processed in
  * chunks of whole set groups, with bitwise the same results (Section IV-B,
- * Chunking).  ENOMEM only when not even one group of 32 sets fits -- the
- * paper's chunk size 0.
+ * Chunking).  ENOMEM only when not even one set group (32 sets, or 16 for
+ * the shapes with 16-wide tiles) fits -- the paper's chunk size 0.
  */
 EXEMCL_API int exemplar_eval(const void *V, int64_t n, int64_t d, const int32_t *sets, int64_t l,
                              int64_t k, int precision, float *out, void *stream);
+
+/*
+ * exemplar_eval_streamed -- exemplar_eval for a V kept in HOST memory, e.g.
+ * one larger than the device's memory.
+ *
+ * The paper keeps V resident on the GPU and splits only the sets into chunks
+ * (Section IV-B, Chunking); that fails once V itself does not fit.  This call
+ * streams V through the device in blocks of rows instead: the set members'
+ * rows are copied once into a compact exemplar matrix and staged, then every
+ * row block is copied in (double-buffered, overlapping the previous block's
+ * kernels) and evaluated by the same kernels as exemplar_eval, and its
+ * per-set sums are added to an fp64 accumulator in block order.  The result
+ * equals f(S_j) up to rounding (within the tolerances of exemplar_eval, not
+ * bitwise equal to it: the summation is grouped by blocks).
+ *
+ *   V               HOST, n x d row-major, type per `precision`; read only.
+ *                   Pinned memory (hipHostMalloc) whose rows are whole
+ *                   16-byte vectors is copied to the device directly; any
+ *                   other host memory goes through the library's pinned
+ *                   staging buffers.
+ *   n, d, l, k      as for exemplar_eval
+ *   sets            HOST, l x k int32 row-major; read only
+ *   precision       one of exemcl_precision
+ *   rows_per_block  ground points per streamed block (rounded up to the
+ *                   kernel's row block); 0 = about 64 MiB of V per block
+ *   out             HOST, l floats; written before the call returns
+ *   stream          hipStream_t or NULL; the kernels run on it, the copies on
+ *                   a second stream of the library's
+ *
+ * Unlike the other entry points this call is synchronous: it returns once
+ * `out` holds the results.  Calls are serialised within a process (they
+ * share the pinned staging buffers, which the library keeps between calls).
+ * Device memory: two row blocks, the compact exemplar matrix and its tiles,
+ * one block's partial sums -- O(rows_per_block * d + l * k * d) bytes, counted
+ * against EXEMCL_WORKSPACE_LIMIT; the sets are not chunked here.
+ * Errors: EINVAL as for exemplar_eval (rows_per_block < 0 too); ENOMEM when
+ * the device or pinned buffers cannot be allocated; EDEVICE when a copy or
+ * launch fails.  Empty slots and invalid indices behave as in exemplar_eval.
+ */
+EXEMCL_API int exemplar_eval_streamed(const void *V, int64_t n, int64_t d, const int32_t *sets, int64_t l,
+                                      int64_t k, int precision, int64_t rows_per_block, float *out,
+                                      void *stream);
 
 /*
  * exemplar_gain -- one Greedy step: f(S u {c}) for every candidate c.

@@ -18,7 +18,8 @@ EXEMCL_OK, EXEMCL_EINVAL, EXEMCL_ENOMEM, EXEMCL_EDEVICE = 0, 1, 2, 3
 PATH_NONE, PATH_VALU, PATH_MFMA = 0, 1, 2
 PATH_NAMES = {PATH_NONE: "none", PATH_VALU: "valu", PATH_MFMA: "mfma"}
 
-EXPORTED = ("exemplar_eval", "exemplar_gain", "exemplar_greedy", "exemplar_sqnorm", "exemplar_plan",
+EXPORTED = ("exemplar_eval", "exemplar_eval_streamed", "exemplar_gain", "exemplar_greedy", "exemplar_sqnorm",
+            "exemplar_plan",
             "exemplar_prof_enable", "exemplar_prof_read", "exemplar_strerror", "exemplar_version")
 
 
@@ -45,6 +46,8 @@ def load(path: str | None = None) -> ctypes.CDLL:
     vp, i64, ip = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int
     lib.exemplar_eval.argtypes = [vp, i64, i64, vp, i64, i64, ip, vp, vp]
     lib.exemplar_eval.restype = ip
+    lib.exemplar_eval_streamed.argtypes = [vp, i64, i64, vp, i64, i64, ip, i64, vp, vp]
+    lib.exemplar_eval_streamed.restype = ip
     lib.exemplar_gain.argtypes = [vp, i64, i64, vp, i64, vp, i64, vp, vp]
     lib.exemplar_gain.restype = ip
     lib.exemplar_greedy.argtypes = [vp, i64, i64, i64, vp, vp, vp]
@@ -127,6 +130,36 @@ def exemplar_eval(V, sets, out=None, stream=None):
         rc = load().exemplar_eval(_ptr(V), n, d, _ptr(sets), l, k, prec, _ptr(out), _stream(stream))
     if rc != EXEMCL_OK:
         raise ExemclError(rc, "exemplar_eval")
+    return out
+
+
+def exemplar_eval_streamed(V, sets, rows_per_block=0, out=None, device=None, stream=None):
+    """out[j] = f(S_j) for V and ``sets`` in host memory (CPU tensors), with V
+    streamed through the GPU in row blocks (see exemplar_eval_streamed in
+    exemcl.h).  Synchronous; returns a CPU float32 tensor.  ``device`` is the
+    GPU to use (default: the current one)."""
+    import torch
+    if V.dim() != 2 or sets.dim() != 2:
+        raise ValueError("V must be n x d and sets l x k")
+    if V.is_cuda or sets.is_cuda:
+        raise ValueError("V and sets must be in host memory")
+    if not V.is_contiguous() or not sets.is_contiguous():
+        raise ValueError("tensors must be contiguous")
+    if sets.dtype != torch.int32:
+        raise TypeError("sets must be int32")
+    prec = precision_of(V.dtype)
+    n, d = V.shape
+    l, k = sets.shape
+    if out is None:
+        out = torch.empty(l, dtype=torch.float32)
+    elif out.is_cuda or out.dtype != torch.float32 or out.numel() != l or not out.is_contiguous():
+        raise ValueError("out must be a contiguous host float32 tensor with l elements")
+    dev = torch.device("cuda", torch.cuda.current_device()) if device is None else torch.device(device)
+    with torch.cuda.device(dev):
+        rc = load().exemplar_eval_streamed(_ptr(V), n, d, _ptr(sets), l, k, prec, int(rows_per_block), _ptr(out),
+                                           _stream(stream))
+    if rc != EXEMCL_OK:
+        raise ExemclError(rc, "exemplar_eval_streamed")
     return out
 
 

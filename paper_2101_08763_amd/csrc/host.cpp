@@ -5,7 +5,9 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <algorithm>
 #include <mutex>
+#include <thread>
 #include <utility>
 #include <vector>
 
@@ -321,6 +323,225 @@ int run_eval(const void *V, int64_t n, int64_t d, const int32_t *sets, int64_t l
     return EXEMCL_OK;
 }
 
+// ---------------------------------------------------------------------------
+// Out-of-core evaluation: V (and the sets) in host memory.
+//
+// The paper keeps V resident on the device and chunks only the sets
+// (Section IV-B, Chunking); its chunking fails once V itself does not fit.
+// Here V streams through the device in blocks of rows: the members of every
+// set are copied once into a compact exemplar matrix and staged into tiles,
+// then each row block is copied in (double-buffered, on a second stream, so
+// the copy of block b + 1 overlaps the kernels of block b), evaluated by the
+// unchanged kernel, and its per-set sums are added to an fp64 accumulator in
+// block order.  The sum over points splits exactly across row blocks, so the
+// result is f(S_j) up to rounding.
+// ---------------------------------------------------------------------------
+
+// Pinned host buffers kept between calls; the mutex also serialises
+// exemplar_eval_streamed within the process.
+std::mutex g_stream_mu;
+struct Pinned {
+    void *p = nullptr;
+    size_t bytes = 0;
+};
+Pinned g_pin_rows[2], g_pin_exem, g_pin_idx, g_pin_bad;
+
+hipError_t pinned_reserve(Pinned *b, size_t bytes) {
+    if (b->bytes >= bytes) return hipSuccess;
+    if (b->p) (void)hipHostFree(b->p);
+    b->p = nullptr;
+    b->bytes = 0;
+    hipError_t e = hipHostMalloc(&b->p, bytes, hipHostMallocDefault);
+    if (e == hipSuccess) b->bytes = bytes;
+    return e;
+}
+
+bool host_is_pinned(const void *p) {
+    hipPointerAttribute_t a{};
+    const hipError_t e = hipPointerGetAttributes(&a, p);
+    if (e != hipSuccess) {
+        (void)hipGetLastError();
+        return false;
+    }
+    return a.type == hipMemoryTypeHost;
+}
+
+// dst rows [0, rows) with stride ld elements <- src rows with stride d,
+// columns d .. ld-1 left as they are; split over a few threads.
+void copy_rows(void *dst, int64_t ld, const void *src, int64_t d, int64_t rows, int64_t es) {
+    const int64_t bytes = rows * d * es;
+    const unsigned hw = std::max(1u, std::thread::hardware_concurrency());
+    const int64_t nt = std::min<int64_t>(std::min<int64_t>(16, hw), std::max<int64_t>(1, bytes >> 22));
+    auto part = [&](int64_t r0, int64_t r1) {
+        if (ld == d) {
+            memcpy((char *)dst + r0 * d * es, (const char *)src + r0 * d * es, (size_t)((r1 - r0) * d * es));
+        } else {
+            for (int64_t r = r0; r < r1; ++r)
+                memcpy((char *)dst + r * ld * es, (const char *)src + r * d * es, (size_t)(d * es));
+        }
+    };
+    if (nt <= 1) {
+        part(0, rows);
+        return;
+    }
+    std::vector<std::thread> th;
+    for (int64_t t = 0; t < nt; ++t) th.emplace_back(part, rows * t / nt, rows * (t + 1) / nt);
+    for (auto &x : th) x.join();
+}
+
+struct StreamedState {
+    hipStream_t cs = nullptr;
+    hipEvent_t copied[2] = {nullptr, nullptr}, freed[2] = {nullptr, nullptr};
+    ~StreamedState() {
+        for (int i = 0; i < 2; ++i) {
+            if (copied[i]) hipEventDestroy(copied[i]);
+            if (freed[i]) hipEventDestroy(freed[i]);
+        }
+        if (cs) hipStreamDestroy(cs);
+    }
+};
+
+int run_streamed(const void *V, int64_t n, int64_t d, const int32_t *sets, int64_t l, int64_t k, int precision,
+                 int64_t rows_per_block, float *out, hipStream_t st) {
+    MfmaPlan mp;
+    if (!mfma_plan(precision, d, &mp)) return EXEMCL_EINVAL;
+    const int64_t es = elem_size(precision);
+    const int64_t ld = mfma_row_stride(precision, d);
+    const int64_t ne = l * k;  // rows of the compact exemplar matrix: member (j, p) is row j*k + p
+    int64_t R = rows_per_block > 0 ? rows_per_block : std::max<int64_t>(1, ((int64_t)64 << 20) / (ld * es));
+    R = std::min(R, n);
+    R = (R + mp.rows - 1) / mp.rows * mp.rows;  // whole row blocks of the kernel
+
+    // Device workspace: 2 row buffers, exemplars, remapped indices, tiles,
+    // one block's partials, the fp64 accumulator, flags and the results.
+    Layout L;
+    if (!layout_eval(R, d, l, k, precision, EXEMCL_PATH_MFMA, &L)) return EXEMCL_EINVAL;
+    const int64_t rows_bytes = align_up(R * ld * es, 256);
+    const int64_t off_rows1 = rows_bytes;
+    const int64_t off_exem = off_rows1 + rows_bytes;
+    const int64_t off_idx = off_exem + align_up(ne * ld * es, 256);
+    const int64_t off_acc = off_idx + align_up(ne * 4, 256);
+    const int64_t off_bad = off_acc + align_up(l * 8, 256);
+    const int64_t off_out = off_bad + align_up(l, 256);
+    const int64_t off_work = off_out + align_up(l * 4, 256);
+    const int64_t bytes = off_work + L.bytes;
+    if (bytes > workspace_limit()) return EXEMCL_ENOMEM;
+
+    std::lock_guard<std::mutex> lk(g_stream_mu);
+    const bool direct = ld == d && host_is_pinned(V);
+    if (pinned_reserve(&g_pin_exem, (size_t)std::max<int64_t>(1, ne * ld * es)) != hipSuccess ||
+        pinned_reserve(&g_pin_idx, (size_t)std::max<int64_t>(1, ne * 4)) != hipSuccess ||
+        pinned_reserve(&g_pin_bad, (size_t)std::max<int64_t>(1, l)) != hipSuccess)
+        return EXEMCL_ENOMEM;
+    if (!direct) {
+        for (int i = 0; i < 2; ++i) {
+            const size_t need = (size_t)(R * ld * es);
+            const bool fresh = g_pin_rows[i].bytes < need;
+            if (pinned_reserve(&g_pin_rows[i], need) != hipSuccess) return EXEMCL_ENOMEM;
+            if (fresh || ld != d) memset(g_pin_rows[i].p, 0, need);  // padding columns stay zero
+        }
+    }
+
+    // Host side of the gather: exemplar rows (zero-padded to ld), indices
+    // remapped into the compact matrix, and the sets with an invalid index.
+    char *E = (char *)g_pin_exem.p;
+    int32_t *ridx = (int32_t *)g_pin_idx.p;
+    uint8_t *bad = (uint8_t *)g_pin_bad.p;
+    auto gather = [&](int64_t j0, int64_t j1) {
+        for (int64_t j = j0; j < j1; ++j) {
+            bad[j] = 0;
+            for (int64_t p = 0; p < k; ++p) {
+                const int64_t i = j * k + p;
+                const int32_t idx = sets[i];
+                char *row = E + i * ld * es;
+                if (idx == kEmptySlot || idx < 0 || idx >= n) {
+                    if (idx != kEmptySlot) bad[j] = 1;
+                    ridx[i] = kEmptySlot;
+                    memset(row, 0, (size_t)(ld * es));
+                } else {
+                    ridx[i] = (int32_t)i;
+                    memcpy(row, (const char *)V + (int64_t)idx * d * es, (size_t)(d * es));
+                    if (ld > d) memset(row + d * es, 0, (size_t)((ld - d) * es));
+                }
+            }
+        }
+    };
+    {
+        const unsigned hw = std::max(1u, std::thread::hardware_concurrency());
+        const int64_t nt = std::min<int64_t>(std::min<int64_t>(16, hw), std::max<int64_t>(1, ne / 2048));
+        if (nt <= 1) {
+            gather(0, l);
+        } else {
+            std::vector<std::thread> th;
+            for (int64_t t = 0; t < nt; ++t) th.emplace_back(gather, l * t / nt, l * (t + 1) / nt);
+            for (auto &x : th) x.join();
+        }
+    }
+
+    Scratch ws;
+    int rc = alloc_scratch(&ws, bytes, st);
+    if (rc) return rc;
+    char *base = (char *)ws.ptr;
+    void *drows[2] = {base, base + off_rows1};
+    void *dexem = base + off_exem;
+    int32_t *didx = (int32_t *)(base + off_idx);
+    double *acc = (double *)(base + off_acc);
+    uint8_t *dbad = (uint8_t *)(base + off_bad);
+    float *dout = (float *)(base + off_out);
+    char *work = base + off_work;
+    float *partials = (float *)(work + L.off_partials);
+    void *tiles = work + L.off_tiles;
+
+    StreamedState ss;
+    if (hipStreamCreateWithFlags(&ss.cs, hipStreamNonBlocking) != hipSuccess) return EXEMCL_EDEVICE;
+    for (int i = 0; i < 2; ++i)
+        if (hipEventCreateWithFlags(&ss.copied[i], hipEventDisableTiming) != hipSuccess ||
+            hipEventCreateWithFlags(&ss.freed[i], hipEventDisableTiming) != hipSuccess)
+            return EXEMCL_EDEVICE;
+
+    hipError_t e = hipMemcpyAsync(dexem, E, (size_t)(ne * ld * es), hipMemcpyHostToDevice, st);
+    if (e == hipSuccess) e = hipMemcpyAsync(didx, ridx, (size_t)(ne * 4), hipMemcpyHostToDevice, st);
+    if (e == hipSuccess) e = hipMemcpyAsync(dbad, bad, (size_t)l, hipMemcpyHostToDevice, st);
+    if (e == hipSuccess) e = launch_pack(precision, mp, dexem, std::max<int64_t>(ne, 1), (int)ld, didx, l, k, tiles, st);
+    // The copy stream may not overwrite a row buffer before the exemplar
+    // upload and tile staging queued above are ordered before it.
+    if (e == hipSuccess) e = hipEventRecord(ss.freed[0], st);
+    if (e == hipSuccess) e = hipEventRecord(ss.freed[1], st);
+    const int64_t nblocks = (n + R - 1) / R;
+    for (int64_t b = 0; b < nblocks && e == hipSuccess; ++b) {
+        const int i = (int)(b & 1);
+        const int64_t r0 = b * R, rows = std::min(R, n - r0);
+        const void *src = (const char *)V + r0 * d * es;
+        if (!direct) {
+            // The pinned buffer of block b - 2 must have reached the device.
+            if (b >= 2) e = hipEventSynchronize(ss.copied[i]);
+            if (e != hipSuccess) break;
+            copy_rows(g_pin_rows[i].p, ld, src, d, rows, es);
+            src = g_pin_rows[i].p;
+        }
+        e = hipStreamWaitEvent(ss.cs, ss.freed[i], 0);
+        if (e == hipSuccess) e = hipMemcpyAsync(drows[i], src, (size_t)(rows * ld * es), hipMemcpyHostToDevice, ss.cs);
+        if (e == hipSuccess) e = hipEventRecord(ss.copied[i], ss.cs);
+        if (e == hipSuccess) e = hipStreamWaitEvent(st, ss.copied[i], 0);
+        Layout Lb;
+        if (e == hipSuccess && !layout_eval(rows, d, l, k, precision, EXEMCL_PATH_MFMA, &Lb)) e = hipErrorInvalidValue;
+        if (e == hipSuccess) {
+            ProfRange pr(st);
+            e = launch_mfma(precision, MODE_SUM, mp, drows[i], rows, (int)ld, tiles, mfma_tiles_per_group(mp, k),
+                            Lb.ngroups, Lb.gpc, nullptr, partials, Lb.lpad, nullptr, st);
+            pr.end();
+        }
+        if (e == hipSuccess) e = launch_accum(partials, Lb.G, Lb.lpad, l, b == 0, acc, st);
+        if (e == hipSuccess) e = hipEventRecord(ss.freed[i], st);
+    }
+    if (e == hipSuccess) e = launch_finish(acc, dbad, l, n, dout, st);
+    if (e == hipSuccess) e = hipMemcpyAsync(out, dout, (size_t)(l * 4), hipMemcpyDeviceToHost, st);
+    const hipError_t es2 = hipStreamSynchronize(st);
+    if (e == hipSuccess) e = es2;
+    (void)hipStreamSynchronize(ss.cs);
+    return status_of(e);
+}
+
 }  // namespace
 
 extern "C" {
@@ -333,6 +554,24 @@ EXEMCL_API int exemplar_eval(const void *V, int64_t n, int64_t d, const int32_t 
     if (l > 0 && k > 0 && !sets) return EXEMCL_EINVAL;
     if (l > 0 && k > 0 && choose_path(d, k, precision) == EXEMCL_PATH_NONE) return EXEMCL_EINVAL;
     return run_eval(V, n, d, sets, l, k, precision, nullptr, nullptr, 0, out, (hipStream_t)stream);
+}
+
+EXEMCL_API int exemplar_eval_streamed(const void *V, int64_t n, int64_t d, const int32_t *sets, int64_t l,
+                                      int64_t k, int precision, int64_t rows_per_block, float *out,
+                                      void *stream) {
+    int rc = check_common(V, n, d, l, k, out);
+    if (rc) return rc;
+    if (!prec_ok(precision)) return EXEMCL_EINVAL;
+    if (l > 0 && k > 0 && !sets) return EXEMCL_EINVAL;
+    if (rows_per_block < 0) return EXEMCL_EINVAL;
+    MfmaPlan mp;
+    if (!mfma_plan(precision, d, &mp)) return EXEMCL_EINVAL;
+    if (l == 0) return EXEMCL_OK;
+    if (k == 0) {  // f(empty) = 0 for every set
+        memset(out, 0, (size_t)l * sizeof(float));
+        return EXEMCL_OK;
+    }
+    return run_streamed(V, n, d, sets, l, k, precision, rows_per_block, out, (hipStream_t)stream);
 }
 
 EXEMCL_API int exemplar_gain(const float *V, int64_t n, int64_t d, const int32_t *S, int64_t k,

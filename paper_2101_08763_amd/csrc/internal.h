@@ -108,6 +108,13 @@ hipError_t launch_reduce(const float *partials, int64_t G, int64_t lpad, int64_t
                          const int32_t *sets, int64_t kset, const int32_t *common, int64_t kcommon, float *out,
                          hipStream_t st);
 
+// Out-of-core evaluation: acc[j] (+)= sum_{g < G} partials[g * lpad + j]
+// (fp64, g in order; `first` overwrites), and out[j] = (2/n) * acc[j], or NaN
+// where bad[j] != 0.
+hipError_t launch_accum(const float *partials, int64_t G, int64_t lpad, int64_t l, bool first, double *acc,
+                        hipStream_t st);
+hipError_t launch_finish(const double *acc, const uint8_t *bad, int64_t l, int64_t n, float *out, hipStream_t st);
+
 hipError_t launch_sqnorm(int prec, const void *V, int64_t n, int d, float *q, hipStream_t st);
 
 // out[i] = 0 for i < count (f of empty sets).

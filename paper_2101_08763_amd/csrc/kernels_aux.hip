@@ -286,6 +286,44 @@ hipError_t launch_zero(float *out, int64_t count, hipStream_t st) {
 }
 
 // ---------------------------------------------------------------------------
+// Out-of-core evaluation: the per-set sums of one block of ground points are
+// added to an fp64 accumulator (acc[j] = sum over blocks in order, each block
+// summed over its partial rows in order), and the accumulator is turned into
+// f(S_j) = (2/n) * acc[j] at the end (NaN for a set with an invalid index).
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void accum_sets_kernel(const float *__restrict__ partials, int64_t G, int64_t lpad,
+                                                          int64_t l, int first, double *__restrict__ acc) {
+    const int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (j >= l) return;
+    double s = 0.0;
+    for (int64_t g = 0; g < G; ++g) s += (double)partials[g * lpad + j];
+    acc[j] = first ? s : acc[j] + s;
+}
+
+hipError_t launch_accum(const float *partials, int64_t G, int64_t lpad, int64_t l, bool first, double *acc,
+                        hipStream_t st) {
+    if (l == 0) return hipSuccess;
+    hipLaunchKernelGGL(accum_sets_kernel, dim3((unsigned)((l + 255) / 256)), dim3(256), 0, st, partials, G, lpad, l,
+                       first ? 1 : 0, acc);
+    return hipGetLastError();
+}
+
+__global__ __launch_bounds__(256) void finish_sets_kernel(const double *__restrict__ acc,
+                                                           const uint8_t *__restrict__ bad, int64_t l, double scale,
+                                                           float *__restrict__ out) {
+    const int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (j >= l) return;
+    out[j] = bad[j] ? __builtin_nanf("") : (float)(scale * acc[j]);
+}
+
+hipError_t launch_finish(const double *acc, const uint8_t *bad, int64_t l, int64_t n, float *out, hipStream_t st) {
+    if (l == 0) return hipSuccess;
+    hipLaunchKernelGGL(finish_sets_kernel, dim3((unsigned)((l + 255) / 256)), dim3(256), 0, st, acc, bad, l,
+                       2.0 / (double)n, out);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
 // q[i] = ||v_i||^2 in fp32, coordinates in order (one thread per point).
 // ---------------------------------------------------------------------------
 template <typename T>

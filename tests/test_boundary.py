@@ -136,3 +136,27 @@ def test_workspace_is_bounded():
     path, ws = api.exemplar_plan(10**6, 256, 2048, 32, api.EXEMCL_FP16)
     assert path == "mfma"
     assert ws < 2048 * 10**6 * 4 / 20
+
+
+# exemplar_eval_streamed takes host arrays: its argument checks and the k = 0
+# case (f(empty) = 0, written on the host) run without a device.
+BAD_STREAMED = BAD_EVAL + [dict(rows_per_block=-1), dict(d=513)]
+
+
+@pytest.mark.parametrize("bad", BAD_STREAMED, ids=[str(b) for b in BAD_STREAMED])
+def test_streamed_rejects(lib, bad):
+    a = dict(V=FAKE, n=100, d=8, sets=FAKE, l=4, k=3, precision=0, rows_per_block=0, out=FAKE)
+    a.update(bad)
+    rc = lib.exemplar_eval_streamed(a["V"], a["n"], a["d"], a["sets"], a["l"], a["k"], a["precision"],
+                                    a["rows_per_block"], a["out"], None)
+    assert rc == api.EXEMCL_EINVAL
+
+
+def test_streamed_empty_sets_on_host(lib):
+    out = (ctypes.c_float * 5)(*([7.0] * 5))
+    V = (ctypes.c_float * 8)()
+    rc = lib.exemplar_eval_streamed(ctypes.cast(V, ctypes.c_void_p), 1, 8, None, 5, 0, 0, 0,
+                                    ctypes.cast(out, ctypes.c_void_p), None)
+    assert rc == api.EXEMCL_OK
+    assert list(out) == [0.0] * 5
+    assert lib.exemplar_eval_streamed(ctypes.cast(V, ctypes.c_void_p), 1, 8, None, 0, 3, 0, 0, None, None) == api.EXEMCL_OK
