@@ -287,6 +287,67 @@ def run_streamed(args, w, dev):
     print(json.dumps(rec), flush=True)
 
 
+def run_greedy(args, w, dev):
+    """Greedy driver (Algorithm 1 on the device): `--greedy-rounds` rounds of
+    scoring every point of V as a candidate, per call.  One JSON line of its
+    own; the oracle baseline scores a sample of candidates against the
+    mid-run solution S_{K/2} on the host cores."""
+    import torch
+    K = args.greedy_rounds
+    log(f"generating {w.name}: {w.note}")
+    p = synth.make(w)
+    V = torch.from_numpy(p.X).to(dev).contiguous()
+    S_out = torch.empty(K, dtype=torch.int32, device=dev)
+    f_out = torch.empty(K, dtype=torch.float32, device=dev)
+    for _ in range(max(args.warmup, 1)):
+        api.exemplar_greedy(V, K, S_out, f_out)
+    torch.cuda.synchronize()
+    api.exemplar_prof_read()
+    api.exemplar_prof_enable(True)
+    stream = torch.cuda.current_stream()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ev0.record(stream)
+    for _ in range(args.steps):
+        api.exemplar_greedy(V, K, S_out, f_out)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    api.exemplar_prof_enable(False)
+    kern_ms, launches = api.exemplar_prof_read()
+    ms = ev0.elapsed_time(ev1) / args.steps
+    n, d = w.n, w.d
+    cand_evals = n * K                      # every point is scored in every round
+    flops = 2.0 * n * n * d * K             # scoring contractions (the cache update is n * d per round)
+    kern_per_call = kern_ms / args.steps
+    rec = {
+        "metric": "greedy rounds/s and candidate evaluations/s (exemplar_greedy, Algorithm 1 on the device)",
+        "value": K / (ms * 1e-3), "unit": "rounds/s", "ms_per_call": ms, "rounds": K, "steps": args.steps,
+        "candidate_evals_per_s": cand_evals / (ms * 1e-3),
+        "scoring_kernel_ms_per_call": kern_per_call, "scoring_launches_per_call": launches / max(args.steps, 1),
+        "roofline": {"bound": "mfma", "achieved": flops / (kern_per_call * 1e-3) / 1e12, "peak": PEAK_TFLOPS["fp32"],
+                     "unit": "TFLOP/s", "frac": flops / (kern_per_call * 1e-3) / 1e12 / PEAK_TFLOPS["fp32"]},
+        "dtype": "f32", "data": "synthetic",
+        "config": {"workload": f"{w.name} points: {w.note}", "n": n, "d": d, "rounds": K},
+        "S": S_out.cpu().tolist(), "f": [float(x) for x in f_out.cpu()],
+    }
+    if not args.no_cpu_baseline:
+        import oracle
+        o = oracle.load()
+        threads = o.threads(0)
+        X64 = p.X.astype(np.float64)
+        half = rec["S"][:K // 2]
+        probe = np.arange(0, n, max(1, n // 16), dtype=np.int32)[:16]
+        t0 = time.perf_counter()
+        o.gain(X64, np.asarray(half, np.int32), probe, threads)
+        dt = time.perf_counter() - t0
+        rec["cpu_baseline"] = {
+            "value": len(probe) / dt, "unit": "candidate evaluations/s", "cores": threads, "kind": "oracle",
+            "sample": f"{len(probe)} candidates scored against S of size {len(half)} (the GPU's first {len(half)} picks), "
+                      f"fp64 direct evaluation, {threads} threads on {cpu_model()}",
+            "seconds": dt,
+        }
+    print(json.dumps(rec), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -308,6 +369,8 @@ def main():
     ap.add_argument("--streamed", action="store_true",
                     help="time exemplar_eval_streamed (V in pinned host memory) instead; one JSON line of its own")
     ap.add_argument("--rows-per-block", type=int, default=0, help="row block of --streamed (0 = library default)")
+    ap.add_argument("--greedy-rounds", type=int, default=0, metavar="K",
+                    help="time exemplar_greedy with K rounds over the workload's points instead (fp32)")
     args = ap.parse_args()
 
     if args.traffic_summary:
@@ -334,6 +397,9 @@ def main():
         return
 
     w = synth.WORKLOADS[args.workload]
+    if args.greedy_rounds > 0:
+        run_greedy(args, w, dev)
+        return
     if args.streamed:
         if w.mode != "eval":
             sys.exit("--streamed evaluates set batches (an eval workload)")
