@@ -367,7 +367,7 @@ bool host_is_pinned(const void *p) {
 }
 
 // dst rows [0, rows) with stride ld elements <- src rows with stride d,
-// columns d .. ld-1 left as they are; split over a few threads.
+// columns d .. ld-1 set to zero; split over a few threads.
 void copy_rows(void *dst, int64_t ld, const void *src, int64_t d, int64_t rows, int64_t es) {
     const int64_t bytes = rows * d * es;
     const unsigned hw = std::max(1u, std::thread::hardware_concurrency());
@@ -376,8 +376,10 @@ void copy_rows(void *dst, int64_t ld, const void *src, int64_t d, int64_t rows, 
         if (ld == d) {
             memcpy((char *)dst + r0 * d * es, (const char *)src + r0 * d * es, (size_t)((r1 - r0) * d * es));
         } else {
-            for (int64_t r = r0; r < r1; ++r)
+            for (int64_t r = r0; r < r1; ++r) {
                 memcpy((char *)dst + r * ld * es, (const char *)src + r * d * es, (size_t)(d * es));
+                memset((char *)dst + (r * ld + d) * es, 0, (size_t)((ld - d) * es));
+            }
         }
     };
     if (nt <= 1) {
@@ -434,12 +436,8 @@ int run_streamed(const void *V, int64_t n, int64_t d, const int32_t *sets, int64
         pinned_reserve(&g_pin_bad, (size_t)std::max<int64_t>(1, l)) != hipSuccess)
         return EXEMCL_ENOMEM;
     if (!direct) {
-        for (int i = 0; i < 2; ++i) {
-            const size_t need = (size_t)(R * ld * es);
-            const bool fresh = g_pin_rows[i].bytes < need;
-            if (pinned_reserve(&g_pin_rows[i], need) != hipSuccess) return EXEMCL_ENOMEM;
-            if (fresh || ld != d) memset(g_pin_rows[i].p, 0, need);  // padding columns stay zero
-        }
+        for (int i = 0; i < 2; ++i)
+            if (pinned_reserve(&g_pin_rows[i], (size_t)(R * ld * es)) != hipSuccess) return EXEMCL_ENOMEM;
     }
 
     // Host side of the gather: exemplar rows (zero-padded to ld), indices
