@@ -30,6 +30,7 @@
 #pragma once
 
 #include <float.h>
+#include <stdlib.h>
 
 #include "device.hpp"
 #include "internal.h"
@@ -133,6 +134,9 @@ __global__ __launch_bounds__(64) void pack_tiles_kernel(const T *__restrict__ V,
 #endif
 #ifndef EXEMCL_PF_SCHED
 #define EXEMCL_PF_SCHED 4
+#endif
+#ifndef EXEMCL_PERSIST_DEFAULT
+#define EXEMCL_PERSIST_DEFAULT 1
 #endif
 #ifndef EXEMCL_SCHED_MIN_NF
 #define EXEMCL_SCHED_MIN_NF 16
@@ -276,8 +280,8 @@ __device__ __forceinline__ void wait_vmcnt() {
 template <typename T, int TILE, int NKB, int NKS_LAST, int RT, int WAVES, int MODE, bool HAS_M0, bool HALF>
 __global__ __launch_bounds__(WAVES * 64) void eval_mfma_kernel(const T *__restrict__ V, int64_t n, int ld,
                                                                  const unsigned char *__restrict__ tiles, int64_t kt,
-                                                                 int64_t ngroups, int64_t gpc,
-                                                                 const float *__restrict__ m0,
+                                                                 int64_t ngroups, int64_t gpc, int64_t nrb,
+                                                                 int persist, const float *__restrict__ m0,
                                                                  float *__restrict__ partials, int64_t lpad,
                                                                  float *__restrict__ rowmax) {
     using M = Mfma<T, TILE>;
@@ -316,9 +320,27 @@ __global__ __launch_bounds__(WAVES * 64) void eval_mfma_kernel(const T *__restri
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
     const int lr = lane % TM, grp = lane / TM;
-    const int64_t rb = blockIdx.x;
-    const int64_t g0 = (int64_t)blockIdx.y * gpc;
-    const int64_t g1 = min(ngroups, g0 + gpc);
+    // Units of work are (row block, set group) pairs, numbered row block
+    // major.  A workgroup takes either one row block and one chunk of gpc
+    // groups (grid = row blocks x chunks), or -- persistent launch, one
+    // workgroup per resident slot -- an equal contiguous range of all
+    // nrb * ngroups units, walked as segments of one row block each.
+    int64_t u0, u1;
+    if (persist) {
+        const int64_t U = nrb * ngroups;
+        u0 = (int64_t)blockIdx.x * U / gridDim.x;
+        u1 = ((int64_t)blockIdx.x + 1) * U / gridDim.x;
+    } else {
+        u0 = (int64_t)blockIdx.x * ngroups + (int64_t)blockIdx.y * gpc;
+        u1 = u0 + min(gpc, ngroups - (int64_t)blockIdx.y * gpc);
+    }
+    for (int64_t u = u0; u < u1;) {
+    const int64_t rb = u / ngroups;
+    const int64_t g0 = u - rb * ngroups;
+    const int64_t g1 = min(ngroups, g0 + (u1 - u));
+    u += g1 - g0;
+    // The previous segment's last stage may still be read by other waves.
+    if (g0 != u0 - (u0 / ngroups) * ngroups || rb != u0 / ngroups) __syncthreads();
     const int64_t row0 = rb * (int64_t)(WAVES * RT * TM) + (int64_t)wave * RT * TM;
 
     const int64_t ntiles = (g1 - g0) * kt;
@@ -608,11 +630,33 @@ __global__ __launch_bounds__(WAVES * 64) void eval_mfma_kernel(const T *__restri
                 }
         }
     }
+    }  // segments
 }
 
 // ---------------------------------------------------------------------------
 // Host-side launch helpers.
 // ---------------------------------------------------------------------------
+// EXEMCL_PERSIST=0 switches the persistent launch off (A/B runs, tests).
+inline bool persistent_launch() {
+    static const int on = [] {
+        const char *s = getenv("EXEMCL_PERSIST");
+        return (s && s[0] == '0') ? 0 : EXEMCL_PERSIST_DEFAULT;
+    }();
+    return on != 0;
+}
+
+// Compute units of the current device (cached per device index).
+inline int64_t device_cu_count() {
+    static int cus[64] = {0};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
+    if (cus[dev] == 0) {
+        int c = 0;
+        if (hipDeviceGetAttribute(&c, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+        cus[dev] = c;
+    }
+    return cus[dev];
+}
 template <typename T, int TILE>
 hipError_t pack_launch(const MfmaPlan &pl, const void *V, int64_t n, int ld, const int32_t *sets, int64_t l,
                        int64_t k, void *tiles, hipStream_t st) {
@@ -640,9 +684,36 @@ hipError_t eval_launch_t(const MfmaArgs &x, hipStream_t st) {
     const int64_t rows = (int64_t)WAVES * RT * TILE;
     const int64_t G = (x.n + rows - 1) / rows;
     const int64_t chunks = (x.ngroups + x.gpc - 1) / x.gpc;
-    hipLaunchKernelGGL(kern, dim3((unsigned)G, (unsigned)chunks), dim3(WAVES * 64), lds, st, (const T *)x.V, x.n,
-                       x.ld, (const unsigned char *)x.tiles, x.kt, x.ngroups, x.gpc, x.m0, x.partials, x.lpad,
-                       x.rowmax);
+    // Persistent launch: as many workgroups as are resident at once, each
+    // with an equal share of the units, so no partly filled last round.
+    // Used for fp32 when there are at least 8 units per slot (fewer cannot
+    // be balanced better than the grid does); not for fp16/bf16, where
+    // workgroups starting at different set groups lose the L2 reuse of the
+    // exemplar tiles that the row-block-major grid keeps (measured), and not
+    // for the row-max mode, whose workgroup must see every group of its row
+    // block.
+    int64_t slots = 0;
+    if (MODE == MODE_SUM && sizeof(T) == 4 && persistent_launch()) {
+        static int per_cu = -1;  // per instantiation; the occupancy does not change
+        if (per_cu < 0) {
+            int nb = 0;
+            if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, (const void *)kern, WAVES * 64, lds) != hipSuccess) {
+                (void)hipGetLastError();
+                nb = 0;
+            }
+            per_cu = nb;
+        }
+        slots = (int64_t)per_cu * device_cu_count();
+    }
+    if (slots > 0 && G * x.ngroups >= 8 * slots) {
+        hipLaunchKernelGGL(kern, dim3((unsigned)slots, 1), dim3(WAVES * 64), lds, st, (const T *)x.V, x.n, x.ld,
+                           (const unsigned char *)x.tiles, x.kt, x.ngroups, x.gpc, G, 1, x.m0, x.partials, x.lpad,
+                           x.rowmax);
+    } else {
+        hipLaunchKernelGGL(kern, dim3((unsigned)G, (unsigned)chunks), dim3(WAVES * 64), lds, st, (const T *)x.V, x.n,
+                           x.ld, (const unsigned char *)x.tiles, x.kt, x.ngroups, x.gpc, G, 0, x.m0, x.partials,
+                           x.lpad, x.rowmax);
+    }
     return hipGetLastError();
 }
 
