@@ -320,27 +320,39 @@ __global__ __launch_bounds__(WAVES * 64) void eval_mfma_kernel(const T *__restri
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
     const int lr = lane % TM, grp = lane / TM;
-    // Units of work are (row block, set group) pairs, numbered row block
-    // major.  A workgroup takes either one row block and one chunk of gpc
-    // groups (grid = row blocks x chunks), or -- persistent launch, one
-    // workgroup per resident slot -- an equal contiguous range of all
-    // nrb * ngroups units, walked as segments of one row block each.
-    int64_t u0, u1;
-    if (persist) {
-        const int64_t U = nrb * ngroups;
-        u0 = (int64_t)blockIdx.x * U / gridDim.x;
-        u1 = ((int64_t)blockIdx.x + 1) * U / gridDim.x;
+    // Units of work are (row block, set group) pairs.  A workgroup takes
+    // either one row block and one chunk of gpc groups (grid = row blocks x
+    // chunks), or -- persistent launch, one workgroup per resident slot, S of
+    // them -- first the whole row blocks w, w + S, w + 2S, ... (q = nrb / S
+    // of them: all workgroups walk the set groups in step, so the exemplar
+    // tiles stay hot in L2), then an equal contiguous share of the units of
+    // the remaining nrb - q*S row blocks (row block major), walked as
+    // segments of one row block each.
+    const int64_t S = gridDim.x;
+    const int64_t q = persist ? nrb / S : 0;
+    const int64_t U2 = persist ? (nrb - q * S) * ngroups : 0;
+    int64_t v = persist ? (int64_t)blockIdx.x * U2 / S : 0;
+    const int64_t v1 = persist ? ((int64_t)blockIdx.x + 1) * U2 / S : 0;
+    for (int64_t seg = 0;; ++seg) {
+    int64_t rb, g0, g1;
+    if (!persist) {
+        if (seg > 0) break;
+        rb = blockIdx.x;
+        g0 = (int64_t)blockIdx.y * gpc;
+        g1 = min(ngroups, g0 + gpc);
+    } else if (seg < q) {
+        rb = seg * S + blockIdx.x;
+        g0 = 0;
+        g1 = ngroups;
     } else {
-        u0 = (int64_t)blockIdx.x * ngroups + (int64_t)blockIdx.y * gpc;
-        u1 = u0 + min(gpc, ngroups - (int64_t)blockIdx.y * gpc);
+        if (v >= v1) break;
+        rb = q * S + v / ngroups;
+        g0 = v - (v / ngroups) * ngroups;
+        g1 = min(ngroups, g0 + (v1 - v));
+        v += g1 - g0;
     }
-    for (int64_t u = u0; u < u1;) {
-    const int64_t rb = u / ngroups;
-    const int64_t g0 = u - rb * ngroups;
-    const int64_t g1 = min(ngroups, g0 + (u1 - u));
-    u += g1 - g0;
     // The previous segment's last stage may still be read by other waves.
-    if (g0 != u0 - (u0 / ngroups) * ngroups || rb != u0 / ngroups) __syncthreads();
+    if (seg > 0) __syncthreads();
     const int64_t row0 = rb * (int64_t)(WAVES * RT * TM) + (int64_t)wave * RT * TM;
 
     const int64_t ntiles = (g1 - g0) * kt;
@@ -685,15 +697,12 @@ hipError_t eval_launch_t(const MfmaArgs &x, hipStream_t st) {
     const int64_t G = (x.n + rows - 1) / rows;
     const int64_t chunks = (x.ngroups + x.gpc - 1) / x.gpc;
     // Persistent launch: as many workgroups as are resident at once, each
-    // with an equal share of the units, so no partly filled last round.
-    // Used for fp32 when there are at least 8 units per slot (fewer cannot
-    // be balanced better than the grid does); not for fp16/bf16, where
-    // workgroups starting at different set groups lose the L2 reuse of the
-    // exemplar tiles that the row-block-major grid keeps (measured), and not
-    // for the row-max mode, whose workgroup must see every group of its row
-    // block.
+    // with an equal share of the units (whole row blocks in step first), so
+    // no partly filled last round.  Used when there are at least 8 units per
+    // slot (fewer cannot be balanced better than the grid does); not for the
+    // row-max mode, whose workgroup must see every group of its row block.
     int64_t slots = 0;
-    if (MODE == MODE_SUM && sizeof(T) == 4 && persistent_launch()) {
+    if (MODE == MODE_SUM && persistent_launch()) {
         static int per_cu = -1;  // per instantiation; the occupancy does not change
         if (per_cu < 0) {
             int nb = 0;
