@@ -29,6 +29,7 @@
 // be copied out of and back into the matrix-core registers at every split.
 #pragma once
 
+#include <atomic>
 #include <float.h>
 #include <stdlib.h>
 
@@ -277,11 +278,12 @@ __device__ __forceinline__ void wait_vmcnt() {
 // MODE_ROWMAX: rowmax[v] = max(m0(v), 0, max over all staged columns of
 // h_s(v)) (m0 = 0 when null); rowmax must not alias m0.
 // ---------------------------------------------------------------------------
-template <typename T, int TILE, int NKB, int NKS_LAST, int RT, int WAVES, int MODE, bool HAS_M0, bool HALF>
-__global__ __launch_bounds__(WAVES * 64) void eval_mfma_kernel(const T *__restrict__ V, int64_t n, int ld,
+template <typename T, int TILE, int NKB, int NKS_LAST, int RT, int WAVES, int MODE, bool HAS_M0, bool HALF,
+          bool PERSIST>
+__global__ __launch_bounds__(WAVES * 64, PERSIST ? 2 : 1) void eval_mfma_kernel(const T *__restrict__ V, int64_t n, int ld,
                                                                  const unsigned char *__restrict__ tiles, int64_t kt,
                                                                  int64_t ngroups, int64_t gpc, int64_t nrb,
-                                                                 int persist, const float *__restrict__ m0,
+                                                                 const float *__restrict__ m0,
                                                                  float *__restrict__ partials, int64_t lpad,
                                                                  float *__restrict__ rowmax) {
     using M = Mfma<T, TILE>;
@@ -317,42 +319,24 @@ __global__ __launch_bounds__(WAVES * 64) void eval_mfma_kernel(const T *__restri
 
     extern __shared__ __align__(16) unsigned char smem[];
 
-    const int tid = threadIdx.x;
-    const int lane = tid & 63, wave = tid >> 6;
-    const int lr = lane % TM, grp = lane / TM;
     // Units of work are (row block, set group) pairs.  A workgroup takes
     // either one row block and one chunk of gpc groups (grid = row blocks x
-    // chunks), or -- persistent launch, one workgroup per resident slot, S of
-    // them -- first the whole row blocks w, w + S, w + 2S, ... (q = nrb / S
-    // of them: all workgroups walk the set groups in step, so the exemplar
-    // tiles stay hot in L2), then an equal contiguous share of the units of
-    // the remaining nrb - q*S row blocks (row block major), walked as
+    // chunks), or -- persistent launch (PERSIST), one workgroup per resident
+    // slot, S of them -- first the whole row blocks w, w + S, w + 2S, ...
+    // (q = nrb / S of them: all workgroups walk the set groups in step, so the
+    // exemplar tiles stay hot in L2), then an equal contiguous share of the
+    // units of the remaining nrb - q*S row blocks (row block major), walked as
     // segments of one row block each.
-    const int64_t S = gridDim.x;
-    const int64_t q = persist ? nrb / S : 0;
-    const int64_t U2 = persist ? (nrb - q * S) * ngroups : 0;
-    int64_t v = persist ? (int64_t)blockIdx.x * U2 / S : 0;
-    const int64_t v1 = persist ? ((int64_t)blockIdx.x + 1) * U2 / S : 0;
-    for (int64_t seg = 0;; ++seg) {
-    int64_t rb, g0, g1;
-    if (!persist) {
-        if (seg > 0) break;
-        rb = blockIdx.x;
-        g0 = (int64_t)blockIdx.y * gpc;
-        g1 = min(ngroups, g0 + gpc);
-    } else if (seg < q) {
-        rb = seg * S + blockIdx.x;
-        g0 = 0;
-        g1 = ngroups;
-    } else {
-        if (v >= v1) break;
-        rb = q * S + v / ngroups;
-        g0 = v - (v / ngroups) * ngroups;
-        g1 = min(ngroups, g0 + (v1 - v));
-        v += g1 - g0;
-    }
-    // The previous segment's last stage may still be read by other waves.
-    if (seg > 0) __syncthreads();
+    // One segment: row block rb, set groups [g0, g1).
+    auto segment = [&](const int64_t rb, const int64_t g0, const int64_t g1) {
+    // Per-lane offsets do not change from one segment to the next; hiding
+    // the thread index and ld per segment keeps the compiler from hoisting
+    // them (RT*NKB load offsets among them) out of the persistent loop,
+    // where they would hold registers through every MFMA chain.
+    int tid = threadIdx.x, ldv = ld;
+    if constexpr (PERSIST) asm volatile("" : "+v"(tid), "+s"(ldv));
+    const int lane = tid & 63, wave = tid >> 6;
+    const int lr = lane % TM, grp = lane / TM;
     const int64_t row0 = rb * (int64_t)(WAVES * RT * TM) + (int64_t)wave * RT * TM;
 
     const int64_t ntiles = (g1 - g0) * kt;
@@ -397,11 +381,11 @@ __global__ __launch_bounds__(WAVES * 64) void eval_mfma_kernel(const T *__restri
 #pragma unroll
         for (int kb = 0; kb < NKF; ++kb) {
             const int d0 = M::dim(kb, grp, 0);
-            a[rt][kb] = window_load16<vec_t>(vwin, d0 < ld ? (uint32_t)((lrow * ld + d0) * (int)sizeof(T)) : kDeadOffset);
+            a[rt][kb] = window_load16<vec_t>(vwin, d0 < ldv ? (uint32_t)((lrow * ldv + d0) * (int)sizeof(T)) : kDeadOffset);
         }
         if constexpr (HALF) {
             const int d0 = M::hdim(NKF, grp, 0);  // ld and d0 are multiples of 4: the 4 elements are in the row
-            ah[rt] = window_load8<hvec_t>(vwin, d0 < ld ? (uint32_t)((lrow * ld + d0) * (int)sizeof(T)) : kDeadOffset);
+            ah[rt] = window_load8<hvec_t>(vwin, d0 < ldv ? (uint32_t)((lrow * ldv + d0) * (int)sizeof(T)) : kDeadOffset);
         }
     }
 
@@ -642,19 +626,51 @@ __global__ __launch_bounds__(WAVES * 64) void eval_mfma_kernel(const T *__restri
                 }
         }
     }
-    }  // segments
+    };
+
+    if constexpr (!PERSIST) {
+        const int64_t g0 = (int64_t)blockIdx.y * gpc;
+        segment((int64_t)blockIdx.x, g0, min(ngroups, g0 + gpc));
+    } else {
+        const int64_t S = gridDim.x;
+        const int64_t q = nrb / S;
+        const int64_t U2 = (nrb - q * S) * ngroups;
+        int64_t v = (int64_t)blockIdx.x * U2 / S;
+        const int64_t v1 = ((int64_t)blockIdx.x + 1) * U2 / S;
+        for (int64_t seg = 0;; ++seg) {
+            int64_t rb, g0, g1;
+            if (seg < q) {
+                rb = seg * S + (int64_t)blockIdx.x;
+                g0 = 0;
+                g1 = ngroups;
+            } else {
+                if (v >= v1) break;
+                rb = q * S + v / ngroups;
+                g0 = v - (v / ngroups) * ngroups;
+                g1 = min(ngroups, g0 + (v1 - v));
+                v += g1 - g0;
+            }
+            // The previous segment's last stage may still be read by other waves.
+            if (seg > 0) __syncthreads();
+            segment(rb, g0, g1);
+        }
+    }
 }
 
 // ---------------------------------------------------------------------------
 // Host-side launch helpers.
 // ---------------------------------------------------------------------------
-// EXEMCL_PERSIST=0 switches the persistent launch off (A/B runs, tests).
-inline bool persistent_launch() {
-    static const int on = [] {
-        const char *s = getenv("EXEMCL_PERSIST");
-        return (s && s[0] == '0') ? 0 : EXEMCL_PERSIST_DEFAULT;
-    }();
-    return on != 0;
+// Launch-mode switch, read on every launch so that tests can flip it:
+// EXEMCL_PERSIST=0 never launches persistently, 2 always does (whenever the
+// mode allows it, however few units there are), anything else (default) uses
+// the rule in eval_launch_t.  0 and 2 exist for A/B runs and for tests that
+// compare both launches bit for bit.
+enum { kPersistOff = 0, kPersistAuto = 1, kPersistForce = 2 };
+inline int persistent_mode() {
+    const char *s = getenv("EXEMCL_PERSIST");
+    if (s && s[0] == '0' && s[1] == '\0') return kPersistOff;
+    if (s && s[0] == '2' && s[1] == '\0') return kPersistForce;
+    return EXEMCL_PERSIST_DEFAULT ? kPersistAuto : kPersistOff;
 }
 
 // Compute units of the current device (cached per device index).
@@ -687,10 +703,13 @@ hipError_t eval_launch_t(const MfmaArgs &x, hipStream_t st) {
     constexpr int TB = tile_bytes_of(hdr_bytes(TILE, NB), HALF ? (NKB - 1) * NB : NF, HALF ? NB : 0);
     constexpr int SB = stage_bytes<TB, NF, WAVES>();
     constexpr int NBUF = ring_depth<TB, NF, WAVES>();
-    auto kern = eval_mfma_kernel<T, TILE, NKB, NKS_LAST, RT, WAVES, MODE, HAS_M0, HALF>;
+    auto kern = eval_mfma_kernel<T, TILE, NKB, NKS_LAST, RT, WAVES, MODE, HAS_M0, HALF, false>;
+    auto kernp = eval_mfma_kernel<T, TILE, NKB, NKS_LAST, RT, WAVES, MODE, HAS_M0, HALF, MODE == MODE_SUM>;
     const size_t lds = (size_t)NBUF * SB;
     if (lds > 64 * 1024) {
         hipError_t e = hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        if (e == hipSuccess && MODE == MODE_SUM)
+            e = hipFuncSetAttribute((const void *)kernp, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
         if (e != hipSuccess) return e;
     }
     const int64_t rows = (int64_t)WAVES * RT * TILE;
@@ -698,30 +717,43 @@ hipError_t eval_launch_t(const MfmaArgs &x, hipStream_t st) {
     const int64_t chunks = (x.ngroups + x.gpc - 1) / x.gpc;
     // Persistent launch: as many workgroups as are resident at once, each
     // with an equal share of the units (whole row blocks in step first), so
-    // no partly filled last round.  Used when there are at least 8 units per
-    // slot (fewer cannot be balanced better than the grid does); not for the
-    // row-max mode, whose workgroup must see every group of its row block.
+    // no partly filled last round.  Not for the row-max mode, whose
+    // workgroup must see every group of its row block.  The rule: at least 8
+    // units per slot (fewer cannot be balanced better than the grid does),
+    // and one workgroup per CU for both variants -- with one workgroup per
+    // CU a CU whose workgroup ends early in the plain grid's last round
+    // idles, while with two a single remaining 4-wavefront workgroup still
+    // keeps every SIMD's matrix core nearly busy, and the plain grid then
+    // measures as fast or faster.
     int64_t slots = 0;
-    if (MODE == MODE_SUM && persistent_launch()) {
-        static int per_cu = -1;  // per instantiation; the occupancy does not change
-        if (per_cu < 0) {
-            int nb = 0;
-            if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, (const void *)kern, WAVES * 64, lds) != hipSuccess) {
+    bool use_persist = false;
+    const int pmode = MODE == MODE_SUM ? persistent_mode() : kPersistOff;
+    if (pmode != kPersistOff) {
+        // Per instantiation: blocks per CU of the persistent and the plain
+        // variant; -1 = not queried yet.  The occupancy does not change.
+        static std::atomic<int> occ_p{-1}, occ_q{-1};
+        int np = occ_p.load(std::memory_order_relaxed), nq = occ_q.load(std::memory_order_relaxed);
+        if (np < 0 || nq < 0) {
+            if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&np, (const void *)kernp, WAVES * 64, lds) != hipSuccess ||
+                hipOccupancyMaxActiveBlocksPerMultiprocessor(&nq, (const void *)kern, WAVES * 64, lds) != hipSuccess) {
                 (void)hipGetLastError();
-                nb = 0;
+                np = nq = 0;
             }
-            per_cu = nb;
+            occ_p.store(np, std::memory_order_relaxed);
+            occ_q.store(nq, std::memory_order_relaxed);
         }
-        slots = (int64_t)per_cu * device_cu_count();
+        slots = (int64_t)np * device_cu_count();
+        if (pmode == kPersistForce) use_persist = slots > 0;
+        else use_persist = slots > 0 && np == 1 && nq == 1 && G * x.ngroups >= 8 * slots;
     }
-    if (slots > 0 && G * x.ngroups >= 8 * slots) {
-        hipLaunchKernelGGL(kern, dim3((unsigned)slots, 1), dim3(WAVES * 64), lds, st, (const T *)x.V, x.n, x.ld,
-                           (const unsigned char *)x.tiles, x.kt, x.ngroups, x.gpc, G, 1, x.m0, x.partials, x.lpad,
+    if (use_persist) {
+        hipLaunchKernelGGL(kernp, dim3((unsigned)slots, 1), dim3(WAVES * 64), lds, st, (const T *)x.V, x.n, x.ld,
+                           (const unsigned char *)x.tiles, x.kt, x.ngroups, x.gpc, G, x.m0, x.partials, x.lpad,
                            x.rowmax);
     } else {
         hipLaunchKernelGGL(kern, dim3((unsigned)G, (unsigned)chunks), dim3(WAVES * 64), lds, st, (const T *)x.V, x.n,
-                           x.ld, (const unsigned char *)x.tiles, x.kt, x.ngroups, x.gpc, G, 0, x.m0, x.partials,
-                           x.lpad, x.rowmax);
+                           x.ld, (const unsigned char *)x.tiles, x.kt, x.ngroups, x.gpc, G, x.m0, x.partials, x.lpad,
+                           x.rowmax);
     }
     return hipGetLastError();
 }
