@@ -145,6 +145,12 @@ __global__ __launch_bounds__(64) void pack_tiles_kernel(const T *__restrict__ V,
 #ifndef EXEMCL_SCHED16
 #define EXEMCL_SCHED16 1
 #endif
+// Tiles of at least EXEMCL_FENCE_MIN_NF fragments (and fewer than
+// EXEMCL_SCHED_MIN_NF) keep their in-tile reads ahead of use with the same
+// scheduling fences, without reads across tiles.
+#ifndef EXEMCL_FENCE_MIN_NF
+#define EXEMCL_FENCE_MIN_NF 4
+#endif
 #ifndef EXEMCL_SCHED32
 #define EXEMCL_SCHED32 0
 #endif
@@ -420,8 +426,9 @@ __global__ __launch_bounds__(WAVES * 64, PERSIST ? 2 : 1) void eval_mfma_kernel(
     // the compiler may not move instructions across k-block boundaries, so
     // the reads stay ahead of their use instead of being sunk next to it;
     // without it every tile starts its own reads (no reads across tiles).
+    constexpr bool FENCE = SCHED || (NF >= EXEMCL_FENCE_MIN_NF && sizeof(T) == 2);
     auto fence = [&]() {
-        if constexpr (SCHED) __builtin_amdgcn_sched_barrier(0);
+        if constexpr (FENCE) __builtin_amdgcn_sched_barrier(0);
     };
     auto head = [&](const unsigned char *tb, vec_t (&bq)[PF], float (&bias)[NB]) {
         const vec_t *B = reinterpret_cast<const vec_t *>(tb + HDR);
