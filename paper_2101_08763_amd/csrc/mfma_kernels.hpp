@@ -682,15 +682,15 @@ inline int persistent_mode() {
 
 // Compute units of the current device (cached per device index).
 inline int64_t device_cu_count() {
-    static int cus[64] = {0};
+    static std::atomic<int> cus[64];  // 0 = not queried yet
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
-    if (cus[dev] == 0) {
-        int c = 0;
+    int c = cus[dev].load(std::memory_order_relaxed);
+    if (c == 0) {
         if (hipDeviceGetAttribute(&c, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
-        cus[dev] = c;
+        cus[dev].store(c, std::memory_order_relaxed);
     }
-    return cus[dev];
+    return c;
 }
 template <typename T, int TILE>
 hipError_t pack_launch(const MfmaPlan &pl, const void *V, int64_t n, int ld, const int32_t *sets, int64_t l,
