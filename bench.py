@@ -41,6 +41,48 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
+# Default warm-up and timed lengths.  The GPU's clock governor needs a few
+# hundred milliseconds of back-to-back work to settle: kernels timed in the
+# first 10-100 calls after idle run up to 10 % slower than under sustained
+# load.  So unless --warmup is given, the warm-up runs untimed steps for
+# WARMUP_SECONDS (at least MIN_WARMUP steps), and unless --steps is given the
+# timed region runs at least MIN_STEPS steps and TIMED_SECONDS.  Explicit
+# values are used exactly.
+WARMUP_SECONDS = 1.0
+MIN_WARMUP = 10
+TIMED_SECONDS = 0.5
+MIN_STEPS = 50
+
+
+def warm_up(step, warmup, sync, seconds=None):
+    """Run the untimed warm-up; return (steps run, seconds per step)."""
+    seconds = WARMUP_SECONDS if seconds is None else seconds
+    sync()
+    t0 = time.perf_counter()
+    if warmup is not None:
+        for _ in range(warmup):
+            step()
+        sync()
+        return warmup, (time.perf_counter() - t0) / max(warmup, 1)
+    n, batch = 0, 1
+    while True:
+        for _ in range(batch):
+            step()
+        n += batch
+        sync()
+        el = time.perf_counter() - t0
+        if el >= seconds and n >= MIN_WARMUP:
+            return n, el / n
+        # about 20 ms of work between synchronisations
+        batch = max(1, min(1000, int(0.02 / max(el / n, 1e-7))))
+
+
+def timed_steps(steps, sec_per_step, min_steps=MIN_STEPS):
+    if steps is not None:
+        return steps
+    return max(min_steps, int(TIMED_SECONDS / max(sec_per_step, 1e-7)) + 1)
+
+
 def cpu_model() -> str:
     try:
         for ln in open("/proc/cpuinfo"):
@@ -202,9 +244,9 @@ def run_paper_sweep(args, dev):
             Xs, _ = synth.rounded(p.X, prec)
             V = (Xs if isinstance(Xs, torch.Tensor) else torch.from_numpy(Xs)).to(dev).contiguous()
             out = torch.empty(l, dtype=torch.float32, device=dev)
-            for _ in range(2):
-                api.exemplar_eval(V, sets, out=out)
-            torch.cuda.synchronize()
+            # the host-side oracle run leaves the GPU idle: let the clocks settle again
+            warm_up(lambda: api.exemplar_eval(V, sets, out=out), None, torch.cuda.synchronize,
+                    seconds=args.sweep_warmup_seconds)
             api.exemplar_prof_read()
             api.exemplar_prof_enable(True)
             evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
@@ -265,22 +307,23 @@ def run_streamed(args, w, dev):
     V = (Xs if isinstance(Xs, torch.Tensor) else torch.from_numpy(Xs)).contiguous().pin_memory()
     S = torch.from_numpy(p.sets).contiguous()
     out = torch.empty(w.l, dtype=torch.float32)
-    for _ in range(max(args.warmup, 1)):
-        api.exemplar_eval_streamed(V, S, rows_per_block=args.rows_per_block, out=out)
+    call = lambda: api.exemplar_eval_streamed(V, S, rows_per_block=args.rows_per_block, out=out)  # noqa: E731
+    warmup, sec = warm_up(call, args.warmup, lambda: None)  # the call is synchronous
+    steps = timed_steps(args.steps, sec, min_steps=5)
     api.exemplar_prof_read()
     api.exemplar_prof_enable(True)
     t0 = time.perf_counter()
-    for _ in range(args.steps):
-        api.exemplar_eval_streamed(V, S, rows_per_block=args.rows_per_block, out=out)
-    dt = (time.perf_counter() - t0) / args.steps
+    for _ in range(steps):
+        call()
+    dt = (time.perf_counter() - t0) / steps
     api.exemplar_prof_enable(False)
     kern_ms, launches = api.exemplar_prof_read()
     vbytes = V.numel() * V.element_size()
     rec = {
         "metric": "set evaluations/s, V streamed from host memory (PCIe-inclusive)",
-        "value": w.l / dt, "unit": "set evaluations/s", "ms_per_call": dt * 1e3, "steps": args.steps,
+        "value": w.l / dt, "unit": "set evaluations/s", "ms_per_call": dt * 1e3, "steps": steps, "warmup": warmup,
         "v_bytes": vbytes, "v_stream_gb_per_s": vbytes / dt / 1e9,
-        "kernel_ms_per_call": kern_ms / max(args.steps, 1), "kernel_launches_per_call": launches / max(args.steps, 1),
+        "kernel_ms_per_call": kern_ms / max(steps, 1), "kernel_launches_per_call": launches / max(steps, 1),
         "rows_per_block": args.rows_per_block, "dtype": DTYPE_NAME[w.precision], "data": "synthetic",
         "config": {"workload": f"{w.name}: {w.note}", "n": w.n, "d": w.d, "l": w.l, "k": w.k},
     }
@@ -299,30 +342,29 @@ def run_greedy(args, w, dev):
     V = torch.from_numpy(p.X).to(dev).contiguous()
     S_out = torch.empty(K, dtype=torch.int32, device=dev)
     f_out = torch.empty(K, dtype=torch.float32, device=dev)
-    for _ in range(max(args.warmup, 1)):
-        api.exemplar_greedy(V, K, S_out, f_out)
-    torch.cuda.synchronize()
+    warmup, sec = warm_up(lambda: api.exemplar_greedy(V, K, S_out, f_out), args.warmup, torch.cuda.synchronize)
+    steps = timed_steps(args.steps, sec, min_steps=3)
     api.exemplar_prof_read()
     api.exemplar_prof_enable(True)
     stream = torch.cuda.current_stream()
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     ev0.record(stream)
-    for _ in range(args.steps):
+    for _ in range(steps):
         api.exemplar_greedy(V, K, S_out, f_out)
     ev1.record(stream)
     torch.cuda.synchronize()
     api.exemplar_prof_enable(False)
     kern_ms, launches = api.exemplar_prof_read()
-    ms = ev0.elapsed_time(ev1) / args.steps
+    ms = ev0.elapsed_time(ev1) / steps
     n, d = w.n, w.d
     cand_evals = n * K                      # every point is scored in every round
     flops = 2.0 * n * n * d * K             # scoring contractions (the cache update is n * d per round)
-    kern_per_call = kern_ms / args.steps
+    kern_per_call = kern_ms / steps
     rec = {
         "metric": "greedy rounds/s and candidate evaluations/s (exemplar_greedy, Algorithm 1 on the device)",
-        "value": K / (ms * 1e-3), "unit": "rounds/s", "ms_per_call": ms, "rounds": K, "steps": args.steps,
+        "value": K / (ms * 1e-3), "unit": "rounds/s", "ms_per_call": ms, "rounds": K, "steps": steps, "warmup": warmup,
         "candidate_evals_per_s": cand_evals / (ms * 1e-3),
-        "scoring_kernel_ms_per_call": kern_per_call, "scoring_launches_per_call": launches / max(args.steps, 1),
+        "scoring_kernel_ms_per_call": kern_per_call, "scoring_launches_per_call": launches / max(steps, 1),
         "roofline": {"bound": "mfma", "achieved": flops / (kern_per_call * 1e-3) / 1e12, "peak": PEAK_TFLOPS["fp32"],
                      "unit": "TFLOP/s", "frac": flops / (kern_per_call * 1e-3) / 1e12 / PEAK_TFLOPS["fp32"]},
         "dtype": "f32", "data": "synthetic",
@@ -351,8 +393,11 @@ def run_greedy(args, w, dev):
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--steps", type=int, default=None,
+                    help=f"timed steps (default: at least {MIN_STEPS} and {TIMED_SECONDS} s of work)")
+    ap.add_argument("--warmup", type=int, default=None,
+                    help=f"untimed warm-up steps (default: {WARMUP_SECONDS} s of back-to-back steps, "
+                         f"at least {MIN_WARMUP})")
     ap.add_argument("--workload", default="mix50k", choices=sorted(synth.WORKLOADS))
     ap.add_argument("--cpu-budget", type=float, default=10.0, help="seconds of oracle time for the CPU baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -366,6 +411,8 @@ def main():
     ap.add_argument("--sweep-reps", type=int, default=15, help="timed calls per sweep point (median reported)")
     ap.add_argument("--sweep-out", metavar="FILE", help="also write the sweep's JSON lines to FILE")
     ap.add_argument("--sweep-cpu-budget", type=float, default=1.0, help="seconds of oracle time per sweep point")
+    ap.add_argument("--sweep-warmup-seconds", type=float, default=0.3,
+                    help="untimed back-to-back calls before each sweep point's timed calls")
     ap.add_argument("--streamed", action="store_true",
                     help="time exemplar_eval_streamed (V in pinned host memory) instead; one JSON line of its own")
     ap.add_argument("--rows-per-block", type=int, default=0, help="row block of --streamed (0 = library default)")
@@ -389,7 +436,7 @@ def main():
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     if args.copy_probe:
-        copy_probe(max(args.steps, 1))
+        copy_probe(args.steps if args.steps else 5)
         return
     api.load()
     if args.sweep:
@@ -426,9 +473,9 @@ def main():
     path, ws = api.exemplar_plan(w.n, w.d, w.l, w.k if w.mode == "eval" else 1, prec_code)
     torch.cuda.synchronize()
 
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
+    warmup, sec_per_step = warm_up(step, args.warmup, torch.cuda.synchronize)
+    steps = timed_steps(args.steps, sec_per_step)
+    log(f"warm-up: {warmup} steps ({warmup * sec_per_step:.2f} s); timing {steps} steps")
     api.exemplar_prof_read()  # drop anything recorded before
 
     stream = torch.cuda.current_stream()
@@ -438,7 +485,7 @@ def main():
     torch.cuda.synchronize()
     ev0.record(stream)
     t0 = time.perf_counter()
-    for _ in range(args.steps):
+    for _ in range(steps):
         step()
     ev1.record(stream)
     torch.cuda.synchronize()
@@ -446,7 +493,7 @@ def main():
     api.exemplar_prof_enable(False)
     kern_ms, launches = api.exemplar_prof_read()
     ms = ev0.elapsed_time(ev1)
-    ms_per_step = ms / args.steps
+    ms_per_step = ms / steps
     kern_avg_ms = kern_ms / max(launches, 1)
 
     value = w.l / (ms_per_step * 1e-3)
@@ -454,7 +501,7 @@ def main():
     flops_per_launch = 2.0 * w.n * contraction_cols * w.d
     achieved = flops_per_launch / (kern_avg_ms * 1e-3) / 1e12
     peak = PEAK_TFLOPS[w.precision]
-    log(f"{args.steps} steps: {ms_per_step * 1e3:.1f} us/step (wall {wall / args.steps * 1e6:.1f} us/step), "
+    log(f"{steps} steps: {ms_per_step * 1e3:.1f} us/step (wall {wall / steps * 1e6:.1f} us/step), "
         f"dominant kernel {kern_avg_ms * 1e3:.1f} us avg over {launches} launches, {achieved:.1f} TFLOP/s")
 
     res = {
@@ -462,8 +509,8 @@ def main():
         "value": value,
         "unit": "set evaluations/s",
         "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
+        "steps": steps,
+        "warmup": warmup,
         "ms_per_step": ms_per_step,
         "higher_is_better": True,
         "scaling": "weak",
