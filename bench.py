@@ -52,6 +52,7 @@ WARMUP_SECONDS = 1.0
 MIN_WARMUP = 10
 TIMED_SECONDS = 0.5
 MIN_STEPS = 50
+PROF_SAMPLES = 100   # launches of the dominant kernel timed with HIP events per run
 
 
 def warm_up(step, warmup, sync, seconds=None):
@@ -481,7 +482,11 @@ def main():
     stream = torch.cuda.current_stream()
     ev0 = torch.cuda.Event(enable_timing=True)
     ev1 = torch.cuda.Event(enable_timing=True)
-    api.exemplar_prof_enable(True)
+    # The dominant kernel's duration comes from HIP events around a sample
+    # of about PROF_SAMPLES launches spread evenly over the timed steps:
+    # recording a pair on every step would slow the steps it measures.
+    prof_every = max(1, steps // PROF_SAMPLES)
+    api.exemplar_prof_enable(prof_every)
     torch.cuda.synchronize()
     ev0.record(stream)
     t0 = time.perf_counter()
@@ -528,6 +533,7 @@ def main():
             "traffic": load_traffic("eval_mfma_kernel" if path == "mfma" else "eval_valu_kernel", w.name),
             "kernel": "eval_mfma_kernel" if path == "mfma" else "eval_valu_kernel",
             "kernel_avg_us": kern_avg_ms * 1e3, "flops_per_launch": flops_per_launch,
+            "timed_launches": launches, "timed_every": prof_every,
         },
     }
     if not args.no_cpu_baseline:

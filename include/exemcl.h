@@ -227,15 +227,17 @@ EXEMCL_API int exemplar_plan(int64_t n, int64_t d, int64_t l, int64_t k, int pre
                              int64_t *workspace_bytes);
 
 /*
- * Profiling hook.  exemplar_prof_enable(1) makes every following
- * exemplar_eval / exemplar_gain call record a pair of HIP events on its
- * stream around its dominant kernel (the contraction + epilogue kernel);
- * exemplar_prof_enable(0) stops recording.  exemplar_prof_read waits for the
- * recorded events, writes the summed kernel time in milliseconds and the
- * number of recorded launches, and forgets them.  Either pointer may be NULL.
- * Meant for benchmarks; recording costs two event records per call.
+ * Profiling hook.  exemplar_prof_enable(N), N >= 1, makes every N-th
+ * following exemplar_eval / exemplar_gain call (the first one included)
+ * record a pair of HIP events on its stream around its dominant kernel (the
+ * contraction + epilogue kernel); exemplar_prof_enable(0) stops recording;
+ * N < 0 is EXEMCL_EINVAL.  exemplar_prof_read waits for the recorded events,
+ * writes the summed kernel time in milliseconds and the number of recorded
+ * launches, and forgets them.  Either pointer may be NULL.  Meant for
+ * benchmarks: each recorded call costs two event records on the stream,
+ * which also delay the kernels after them, so long runs sample (N > 1).
  */
-EXEMCL_API int exemplar_prof_enable(int on);
+EXEMCL_API int exemplar_prof_enable(int every);
 EXEMCL_API int exemplar_prof_read(double *ms_total, int64_t *launches);
 
 /* exemplar_strerror -- static, NUL-terminated text for a status code. */

@@ -230,9 +230,14 @@ def exemplar_plan(n: int, d: int, l: int, k: int, precision: int = EXEMCL_FP32):
     return PATH_NAMES.get(path.value, str(path.value)), int(ws.value)
 
 
-def exemplar_prof_enable(on: bool = True) -> None:
-    """Record HIP events around the dominant kernel of every following call."""
-    load().exemplar_prof_enable(1 if on else 0)
+def exemplar_prof_enable(on=True) -> None:
+    """Record HIP events around the dominant kernel of following calls:
+    True or 1 = every call, an integer N > 1 = every N-th call (the first
+    included), False or 0 = stop."""
+    every = int(on) if not isinstance(on, bool) else (1 if on else 0)
+    rc = load().exemplar_prof_enable(every)
+    if rc != EXEMCL_OK:
+        raise ExemclError(rc, "exemplar_prof_enable")
 
 
 def exemplar_prof_read():

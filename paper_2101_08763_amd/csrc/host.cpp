@@ -208,7 +208,8 @@ int prepare_rows(const void *V, int64_t n, int64_t d, int precision, hipStream_t
 
 // Event pairs around the dominant kernel, recorded while profiling is on.
 std::mutex g_prof_mu;
-bool g_prof_on = false;
+int g_prof_every = 0;    // record every g_prof_every-th call; 0 = off
+int64_t g_prof_calls = 0;  // calls seen since recording was switched on
 std::vector<std::pair<hipEvent_t, hipEvent_t>> g_prof_events;
 
 struct ProfRange {
@@ -218,7 +219,7 @@ struct ProfRange {
         bool on;
         {
             std::lock_guard<std::mutex> lk(g_prof_mu);
-            on = g_prof_on;
+            on = g_prof_every > 0 && g_prof_calls++ % g_prof_every == 0;
         }
         if (!on) return;
         if (hipEventCreate(&a) != hipSuccess || hipEventCreate(&b) != hipSuccess) {
@@ -709,9 +710,11 @@ EXEMCL_API int exemplar_plan(int64_t n, int64_t d, int64_t l, int64_t k, int pre
     return EXEMCL_OK;
 }
 
-EXEMCL_API int exemplar_prof_enable(int on) {
+EXEMCL_API int exemplar_prof_enable(int every) {
+    if (every < 0) return EXEMCL_EINVAL;
     std::lock_guard<std::mutex> lk(g_prof_mu);
-    g_prof_on = on != 0;
+    g_prof_every = every;
+    g_prof_calls = 0;
     return EXEMCL_OK;
 }
 

@@ -160,3 +160,16 @@ def test_streamed_empty_sets_on_host(lib):
     assert rc == api.EXEMCL_OK
     assert list(out) == [0.0] * 5
     assert lib.exemplar_eval_streamed(ctypes.cast(V, ctypes.c_void_p), 1, 8, None, 0, 3, 0, 0, None, None) == api.EXEMCL_OK
+
+
+def test_prof_enable_arguments(lib):
+    """Profiling switch: N >= 0 accepted, N < 0 rejected; reading with no
+    recorded launches gives zeros (no device work)."""
+    assert lib.exemplar_prof_enable(-1) == api.EXEMCL_EINVAL
+    assert lib.exemplar_prof_enable(7) == api.EXEMCL_OK
+    assert lib.exemplar_prof_enable(0) == api.EXEMCL_OK
+    ms, cnt = ctypes.c_double(1.0), ctypes.c_int64(5)
+    assert lib.exemplar_prof_read(ctypes.byref(ms), ctypes.byref(cnt)) == api.EXEMCL_OK
+    assert ms.value == 0.0 and cnt.value == 0
+    with pytest.raises(api.ExemclError):
+        api.exemplar_prof_enable(-2)

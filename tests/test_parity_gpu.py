@@ -395,3 +395,23 @@ def test_chunked_gain(torch_gpu, monkeypatch):
     monkeypatch.setenv("EXEMCL_WORKSPACE_LIMIT", str(ws // 4))
     chunked = api.exemplar_gain(Vg, S, C).cpu().numpy()
     assert np.array_equal(full, chunked)
+
+
+def test_prof_samples_every_nth_call(torch_gpu):
+    """exemplar_prof_enable(N) records the dominant kernel of calls 0, N, 2N, ..."""
+    torch = torch_gpu
+    p = synth.random_problem(3000, 40, 64, 6, seed=51)
+    Vg, _ = to_gpu(torch, p.X, "fp32")
+    s = torch.from_numpy(p.sets).cuda()
+    api.exemplar_prof_read()
+    api.exemplar_prof_enable(3)
+    for _ in range(7):
+        api.exemplar_eval(Vg, s)
+    api.exemplar_prof_enable(False)
+    ms, launches = api.exemplar_prof_read()
+    assert launches == 3 and ms > 0.0
+    api.exemplar_prof_enable(True)
+    for _ in range(2):
+        api.exemplar_eval(Vg, s)
+    api.exemplar_prof_enable(False)
+    assert api.exemplar_prof_read()[1] == 2
