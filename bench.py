@@ -141,11 +141,18 @@ def cpu_baseline(p: synth.Problem, X64: np.ndarray, budget_s: float):
     }
 
 
+# Files that define the evaluation kernels and their launch geometry (host
+# glue such as host.cpp, and the greedy kernels, do not change what the
+# traffic counters of eval_mfma_kernel / eval_valu_kernel read).
+KERNEL_FILES = ["device.hpp", "internal.h", "kernels_aux.hip", "kernels_mfma.hip", "kernels_mfma_bf16.hip",
+                "kernels_mfma_f16.hip", "kernels_mfma_f32.hip", "mfma_kernels.hpp", "../build.py"]
+
+
 def kernel_source_hash() -> str:
     """Hash of everything that defines the compiled kernels (sources, build flags)."""
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2101_08763_amd", "csrc")
-    for f in sorted(os.listdir(csrc)) + ["../build.py"]:
+    for f in KERNEL_FILES:
         with open(os.path.join(csrc, f), "rb") as fh:
             h.update(f.encode())
             h.update(fh.read())
