@@ -25,6 +25,7 @@ struct MfmaPlan {
     int kb_dims;    // coordinates per k-block
     int nb;         // set members per staged tile (a set group spans ceil(k / nb) tiles)
     int half;       // 1: the last k-block holds 16 coordinates (16x16x16 instruction)
+    int splat;      // 1: tile headers hold bf16 bias parts for the splat MFMA (32x32x16, few k-blocks)
 };
 
 bool mfma_plan(int prec, int64_t d, MfmaPlan *p);

@@ -38,6 +38,7 @@ bool mfma_plan(int prec, int64_t d, MfmaPlan *p) {
     q.waves = 4;
     q.nb = 1;
     q.half = 0;
+    q.splat = 0;
     if (prec == P_FP32 && d <= 256) {
         // v_mfma_f32_32x32x2_f32, 8 coordinates per k-block
         q.tile = 32;
@@ -73,12 +74,14 @@ bool mfma_plan(int prec, int64_t d, MfmaPlan *p) {
     q.rt = plan_rt(eb, q.tile, q.nkb);
     q.waves = plan_waves(eb, q.tile, q.nkb);
     q.rows = q.waves * q.rt * q.tile;
+    q.splat = splat_bias(eb, q.tile, q.nkb) ? 1 : 0;
     *p = q;
     return true;
 }
 
 int64_t mfma_tile_bytes(const MfmaPlan &pl) {
-    return hdr_bytes(pl.tile, pl.nb) + (int64_t)(pl.nkb - pl.half) * pl.nb * 1024 + (int64_t)pl.half * pl.nb * 512;
+    return hdr_bytes(pl.tile, pl.nb, pl.splat != 0) + (int64_t)(pl.nkb - pl.half) * pl.nb * 1024 +
+           (int64_t)pl.half * pl.nb * 512;
 }
 
 int64_t mfma_tiles_per_group(const MfmaPlan &pl, int64_t k) { return (k + pl.nb - 1) / pl.nb; }

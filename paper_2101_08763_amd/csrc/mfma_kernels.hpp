@@ -38,9 +38,28 @@
 
 namespace exemcl {
 
+// 32x32x16 fp16/bf16 tiles of at most EXEMCL_SPLAT_MAX_NKB k-blocks seed
+// their accumulators with the bias by one bf16 MFMA (see eval_mfma_kernel);
+// their header holds each column's bias as three bf16 parts.
+#ifndef EXEMCL_SPLAT_MFMA
+#define EXEMCL_SPLAT_MFMA 1
+#endif
+#ifndef EXEMCL_SPLAT_MAX_NKB
+#define EXEMCL_SPLAT_MAX_NKB 4
+#endif
+constexpr bool splat_bias(int elem_bytes, int tile, int nkb) {
+    return EXEMCL_SPLAT_MFMA && elem_bytes == 2 && tile == 32 && nkb <= EXEMCL_SPLAT_MAX_NKB;
+}
+
+// Largest finite bf16 (0x7F7F).
+constexpr float kBf16Max = 3.38953139e38f;
+
 // Tile header: the TM * NB fp32 biases of a tile's columns, padded to a
-// multiple of 128 bytes.
-constexpr int hdr_bytes(int tm, int nb) { return (tm * nb * 4 + 127) / 128 * 128; }
+// multiple of 128 bytes; with `splat` (NB = 1), column c's bias as bf16
+// (hi, mid, lo, 0) at byte 8c, 256 bytes.
+constexpr int hdr_bytes(int tm, int nb, bool splat = false) {
+    return splat ? (tm * 8 + 127) / 128 * 128 : (tm * nb * 4 + 127) / 128 * 128;
+}
 
 // Bytes of a staged tile: header, NFF whole fragments of 1 KiB and, when the
 // last k-block is a half one, NB half fragments of 512 bytes.
@@ -54,7 +73,10 @@ constexpr int tile_bytes_of(int hdr, int nff, int nhalf) { return hdr + nff * 10
 // member q*NB + h in column group h.  Byte layout of one tile
 // (HDR + nkb * NB * 1024 bytes):
 //   [0, HDR)                         TM*NB fp32 biases -||s||^2/2, column
-//                                    c of group h at index h*TM + c
+//                                    c of group h at index h*TM + c (with
+//                                    `splat`: column c's bias as bf16
+//                                    hi, mid, lo, 0 at byte 8c, where
+//                                    hi + mid + lo equals the fp32 bias)
 //   [HDR + (kb*NB + h)*1024 + 16*L)  lane L's 16-byte B-operand vector for
 //                                    k-block kb of column group h
 // Padding columns (set >= l), members past k, empty slots and invalid
@@ -66,7 +88,7 @@ constexpr int tile_bytes_of(int hdr, int nff, int nhalf) { return hdr + nff * 10
 template <typename T, int TILE>
 __global__ __launch_bounds__(64) void pack_tiles_kernel(const T *__restrict__ V, int64_t n, int ld,
                                                         const int32_t *__restrict__ sets, int64_t l,
-                                                        int64_t k, int nkb, int half,
+                                                        int64_t k, int nkb, int half, int splat,
                                                         unsigned char *__restrict__ tiles) {
     using M = Mfma<T, TILE>;
     constexpr int NB = M::NB;
@@ -76,7 +98,7 @@ __global__ __launch_bounds__(64) void pack_tiles_kernel(const T *__restrict__ V,
     const int lane = threadIdx.x;
     const int col = lane % M::TM, grp = lane / M::TM;
     const int64_t j = g * M::TM + col;
-    constexpr int HDR = hdr_bytes(M::TM, NB);
+    const int HDR = hdr_bytes(M::TM, NB, splat != 0);
     const int nfull = nkb - half;  // whole k-blocks; a half one follows when half = 1
     unsigned char *tile = tiles + t * (int64_t)tile_bytes_of(HDR, nfull * NB, half * NB);
     typename M::vec_t *dst = reinterpret_cast<typename M::vec_t *>(tile + HDR);
@@ -118,7 +140,28 @@ __global__ __launch_bounds__(64) void pack_tiles_kernel(const T *__restrict__ V,
         }
 #pragma unroll
         for (int off = M::TM; off < 64; off <<= 1) sq += __shfl_xor(sq, off);
-        if (grp == 0) reinterpret_cast<float *>(tile)[h * M::TM + col] = valid ? -0.5f * sq : -FLT_MAX;
+        const float b = valid ? -0.5f * sq : -FLT_MAX;
+        if (grp == 0) {
+            if (sizeof(T) == 2 && splat) {
+                // Exact three-way split: hi is b rounded to bf16, mid the
+                // rest rounded again, lo what is left (8 bits at most), so
+                // hi + mid + lo == b.  Clamped to a finite value first, so a
+                // zero operand times any part is 0.
+                const float bc = fmaxf(b, -kBf16Max);
+                const __bf16 hi = (__bf16)bc;
+                const float r1 = bc - (float)hi;
+                const __bf16 mid = (__bf16)r1;
+                const __bf16 lo = (__bf16)(r1 - (float)mid);
+                bf16x4 hv;
+                hv[0] = hi;
+                hv[1] = mid;
+                hv[2] = lo;
+                hv[3] = (__bf16)0.0f;
+                reinterpret_cast<bf16x4 *>(tile)[col] = hv;
+            } else {
+                reinterpret_cast<float *>(tile)[h * M::TM + col] = b;
+            }
+        }
     }
 }
 
@@ -302,7 +345,15 @@ __global__ __launch_bounds__(WAVES * 64, PERSIST ? 2 : 1) void eval_mfma_kernel(
     // (512 bytes each) follow the NFF whole ones and bypass the prefetch ring.
     constexpr int NFF = HALF ? (NKB - 1) * NB : NF;
     constexpr int NT = WAVES * 64;
-    constexpr int HDR = hdr_bytes(TM, NB);
+    // Short 32x32x16 fp16/bf16 tiles are bound by VALU work, much of it the
+    // 16-register bias splat that seeds each tile's accumulators.  There
+    // (SPLAT) the header holds every column's bias as three bf16 parts and
+    // one bf16 MFMA of a ones operand (coordinates 0-2 of the lanes of
+    // K-group 0, zero elsewhere) against them builds the splat exactly on
+    // the matrix cores; the VALU only folds.
+    constexpr bool SPLAT = splat_bias((int)sizeof(T), TILE, NKB);
+    constexpr int NBIAS = SPLAT ? 2 : NB;  // bias registers per tile (SPLAT: the 8 header bytes)
+    constexpr int HDR = hdr_bytes(TM, NB, SPLAT);
     constexpr int TB = tile_bytes_of(HDR, NFF, HALF ? NB : 0);
     constexpr int SB = stage_bytes<TB, NF, WAVES>();
     constexpr int TPS = tiles_per_stage<TB, NF, WAVES>();
@@ -317,8 +368,12 @@ __global__ __launch_bounds__(WAVES * 64, PERSIST ? 2 : 1) void eval_mfma_kernel(
     // divides NF; the next tile then finds fragment i in slot i.
     constexpr int PF = SCHED ? prefetch_depth(NF, EXEMCL_PF_SCHED) : (NFF < EXEMCL_PF ? NFF : EXEMCL_PF);
     static_assert(!SCHED || NF % PF == 0, "cross-tile prefetch ring must wrap at the tile end");
+    static_assert(!SPLAT || (!SCHED && NB == 1 && !HALF && MODE == MODE_SUM && !HAS_M0), "splat tiles");
     static_assert(MODE == MODE_SUM || NB == 1, "the row-max mode stages one member per tile");
-    constexpr bool PAIR = EXEMCL_PAIR && NB == 1 && NKB <= (sizeof(T) == 4 ? EXEMCL_PAIR_NKB32 : EXEMCL_PAIR_NKB16);
+    // Pairs of tiles per fold (not for HAS_M0: the scoring of S u {c} has
+    // single-member sets, where every tile is a set group of its own).
+    constexpr bool PAIR = EXEMCL_PAIR && NB == 1 && !HAS_M0 &&
+                          NKB <= (sizeof(T) == 4 ? EXEMCL_PAIR_NKB32 : EXEMCL_PAIR_NKB16);
     static_assert(TPS >= 1 && TPS * TB <= SB && NBUF >= 2 && NBUF * SB <= kLdsBytes, "stage geometry");
     static_assert(CNT * (NBUF - 2) < 64, "vmcnt range");
     static_assert(NKS_LAST >= 1 && NKS_LAST <= M::KS_PER_KB, "k-steps of the last block");
@@ -430,24 +485,46 @@ __global__ __launch_bounds__(WAVES * 64, PERSIST ? 2 : 1) void eval_mfma_kernel(
     auto fence = [&]() {
         if constexpr (FENCE) __builtin_amdgcn_sched_barrier(0);
     };
-    auto head = [&](const unsigned char *tb, vec_t (&bq)[PF], float (&bias)[NB]) {
+    auto head = [&](const unsigned char *tb, vec_t (&bq)[PF], float (&bias)[NBIAS]) {
         const vec_t *B = reinterpret_cast<const vec_t *>(tb + HDR);
 #pragma unroll
         for (int i = 0; i < PF; ++i) bq[i] = B[i * 64 + lane];
+        if constexpr (SPLAT) {
+            // every lane reads its column's parts; K-group 1 multiplies them by 0
+            bias[0] = reinterpret_cast<const float *>(tb)[2 * lr];
+            bias[1] = reinterpret_cast<const float *>(tb)[2 * lr + 1];
+        } else {
 #pragma unroll
-        for (int h = 0; h < NB; ++h) bias[h] = reinterpret_cast<const float *>(tb)[h * TM + lr];
+            for (int h = 0; h < NB; ++h) bias[h] = reinterpret_cast<const float *>(tb)[h * TM + lr];
+        }
     };
-    auto chain = [&](const unsigned char *tb, const unsigned char *tnext, vec_t (&bq)[PF], float (&bias)[NB],
+    // The ones operand of the splat MFMA: bf16 1.0 in elements 0-2 of the
+    // K-group 0 lanes.
+    u32x4 ones_w = {0u, 0u, 0u, 0u};
+    if (SPLAT && grp == 0) {
+        ones_w[0] = 0x3F803F80u;
+        ones_w[1] = 0x00003F80u;
+    }
+    const bf16x8 ones = __builtin_bit_cast(bf16x8, ones_w);
+    auto chain = [&](const unsigned char *tb, const unsigned char *tnext, vec_t (&bq)[PF], float (&bias)[NBIAS],
                      acc_t (&acc)[RT][NB]) {
         if constexpr (!SCHED) head(tb, bq, bias);
         const vec_t *B = reinterpret_cast<const vec_t *>(tb + HDR);
         const vec_t *Bn = reinterpret_cast<const vec_t *>(tnext + HDR);
+        if constexpr (SPLAT) {
+            u32x4 w = {__builtin_bit_cast(uint32_t, bias[0]), __builtin_bit_cast(uint32_t, bias[1]), 0u, 0u};
+            const acc_t seed = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ones, __builtin_bit_cast(bf16x8, w), acc_t{},
+                                                                       0, 0, 0);
 #pragma unroll
-        for (int rt = 0; rt < RT; ++rt)
+            for (int rt = 0; rt < RT; ++rt) acc[rt][0] = seed;
+        } else {
 #pragma unroll
-            for (int h = 0; h < NB; ++h)
+            for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
-                for (int i = 0; i < M::ACC; ++i) acc[rt][h][i] = bias[h];
+                for (int h = 0; h < NB; ++h)
+#pragma unroll
+                    for (int i = 0; i < M::ACC; ++i) acc[rt][h][i] = bias[h];
+        }
         float bias_next[NB];
 #pragma unroll
         for (int h = 0; h < NB; ++h) bias_next[h] = 0.0f;
@@ -497,31 +574,27 @@ __global__ __launch_bounds__(WAVES * 64, PERSIST ? 2 : 1) void eval_mfma_kernel(
             for (int h = 0; h < NB; ++h) bias[h] = bias_next[h];
         }
     };
-    // m = max(m, every column group of x): with NB = 2 one max3 per element.
-    // A set group's first tile folds against the initial value instead, so
-    // the running max needs no reset between groups (MODE_SUM; MODE_ROWMAX
-    // keeps one running max over everything staged).
-    auto fold_from = [&](const acc_t (&x)[RT][NB], auto start) {
+    // m = max(m, every column group of x), in place: with NB = 2 one max3
+    // per element.  After each set group's sum the running max goes back to
+    // its initial value (MODE_SUM; MODE_ROWMAX keeps one running max over
+    // everything staged).
+    auto fold = [&](const acc_t (&x)[RT][NB]) {
 #pragma unroll
         for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
             for (int i = 0; i < M::ACC; ++i) {
-                float v = start(rt, i);
+                float v = m[rt][i];
 #pragma unroll
                 for (int h = 0; h < NB; ++h) v = fmaxf(v, x[rt][h][i]);
                 m[rt][i] = v;
             }
     };
-    auto fold = [&](const acc_t (&x)[RT][NB], bool first) {
-        if (first) fold_from(x, m_init);  // uniform branch: two straight-line variants
-        else fold_from(x, [&](int rt, int i) { return m[rt][i]; });
-    };
     // Two single-member tiles of the same set group (NB = 1): one max3.
-    auto fold2_from = [&](const acc_t (&x)[RT][NB], const acc_t (&y)[RT][NB], auto start) {
+    auto fold2 = [&](const acc_t (&x)[RT][NB], const acc_t (&y)[RT][NB]) {
 #pragma unroll
         for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
-            for (int i = 0; i < M::ACC; ++i) m[rt][i] = fmaxf(fmaxf(start(rt, i), x[rt][0][i]), y[rt][0][i]);
+            for (int i = 0; i < M::ACC; ++i) m[rt][i] = fmaxf(fmaxf(m[rt][i], x[rt][0][i]), y[rt][0][i]);
     };
     // Sum of this lane's running maxima in a fixed pairwise order.
     auto lane_sum = [&]() {
@@ -557,9 +630,9 @@ __global__ __launch_bounds__(WAVES * 64, PERSIST ? 2 : 1) void eval_mfma_kernel(
         const int tn = (int)min((int64_t)TPS, ntiles - (int64_t)s * TPS);
         auto tile_at = [&](int i) { return buf + (i < tn ? i : tn - 1) * TB; };
         vec_t bq[PF];
-        float bias[NB];
+        float bias[NBIAS];
 #pragma unroll
-        for (int h = 0; h < NB; ++h) bias[h] = 0.0f;
+        for (int h = 0; h < NBIAS; ++h) bias[h] = 0.0f;
         if constexpr (SCHED) head(buf, bq, bias);
         // Close set group g after its last tile: sum this lane's rows for
         // its column, then the K-groups holding the other rows of the same
@@ -570,27 +643,31 @@ __global__ __launch_bounds__(WAVES * 64, PERSIST ? 2 : 1) void eval_mfma_kernel(
 #pragma unroll
                 for (int off = TM; off < 64; off <<= 1) sum += __shfl_xor(sum, off);
                 if (grp == 0) wpart[(int64_t)g * TM + lr] = sum;
+#pragma unroll
+                for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+                    for (int i = 0; i < M::ACC; ++i) m[rt][i] = m_init(rt, i);
             }
         };
         if constexpr (PAIR) {
+            // One fold site per iteration, so the running max stays in one
+            // set of registers (with two sites the compiler copies it back
+            // every iteration): two members of the same set group when this
+            // stage holds both, else the lone member folded with itself.
             int tt = 0;
             while (tt < tn) {
-                if (tt + 1 < tn && p + 1 < ktile) {
-                    // Two members of the same set group: one max3 per element.
-                    acc_t x[RT][NB], y[RT][NB];
-                    chain(tile_at(tt), tile_at(tt + 1), bq, bias, x);
+                const bool two = tt + 1 < tn && p + 1 < ktile;
+                acc_t x[RT][NB], y[RT][NB];
+                chain(tile_at(tt), tile_at(tt + 1), bq, bias, x);
+                if (two) {
                     chain(tile_at(tt + 1), tile_at(tt + 2), bq, bias, y);
-                    if (MODE == MODE_SUM && p == 0) fold2_from(x, y, m_init);
-                    else fold2_from(x, y, [&](int rt, int i) { return m[rt][i]; });
-                    tt += 2;
-                    p += 2;
                 } else {
-                    acc_t x[RT][NB];
-                    chain(tile_at(tt), tile_at(tt + 1), bq, bias, x);
-                    fold(x, MODE == MODE_SUM && p == 0);
-                    tt += 1;
-                    p += 1;
+#pragma unroll
+                    for (int rt = 0; rt < RT; ++rt) y[rt][0] = x[rt][0];
                 }
+                fold2(x, y);
+                tt += two ? 2 : 1;
+                p += two ? 2 : 1;
                 if (p == ktile) {
                     group_end();
                     p = 0;
@@ -601,7 +678,7 @@ __global__ __launch_bounds__(WAVES * 64, PERSIST ? 2 : 1) void eval_mfma_kernel(
             for (int tt = 0; tt < tn; ++tt) {
                 acc_t x[RT][NB];
                 chain(tile_at(tt), tile_at(tt + 1), bq, bias, x);
-                fold(x, MODE == MODE_SUM && p == 0);
+                fold(x);
                 if (++p == ktile) {
                     group_end();
                     p = 0;
@@ -696,10 +773,11 @@ template <typename T, int TILE>
 hipError_t pack_launch(const MfmaPlan &pl, const void *V, int64_t n, int ld, const int32_t *sets, int64_t l,
                        int64_t k, void *tiles, hipStream_t st) {
     if (pl.half && !Mfma<T, TILE>::HAS_HALF) return hipErrorInvalidValue;
+    if ((pl.splat != 0) != splat_bias((int)sizeof(T), TILE, pl.nkb)) return hipErrorInvalidValue;
     const int64_t ngroups = (l + TILE - 1) / TILE;
     const int64_t kt = (k + Mfma<T, TILE>::NB - 1) / Mfma<T, TILE>::NB;
     hipLaunchKernelGGL((pack_tiles_kernel<T, TILE>), dim3((unsigned)(ngroups * kt)), dim3(64), 0, st,
-                       (const T *)V, n, ld, sets, l, k, pl.nkb, pl.half, (unsigned char *)tiles);
+                       (const T *)V, n, ld, sets, l, k, pl.nkb, pl.half, pl.splat, (unsigned char *)tiles);
     return hipGetLastError();
 }
 
@@ -707,7 +785,8 @@ template <typename T, int TILE, int NKB, int NKS_LAST, int RT, int WAVES, int MO
 hipError_t eval_launch_t(const MfmaArgs &x, hipStream_t st) {
     constexpr int NB = Mfma<T, TILE>::NB;
     constexpr int NF = NKB * NB;
-    constexpr int TB = tile_bytes_of(hdr_bytes(TILE, NB), HALF ? (NKB - 1) * NB : NF, HALF ? NB : 0);
+    constexpr int TB = tile_bytes_of(hdr_bytes(TILE, NB, splat_bias((int)sizeof(T), TILE, NKB)),
+                                     HALF ? (NKB - 1) * NB : NF, HALF ? NB : 0);
     constexpr int SB = stage_bytes<TB, NF, WAVES>();
     constexpr int NBUF = ring_depth<TB, NF, WAVES>();
     auto kern = eval_mfma_kernel<T, TILE, NKB, NKS_LAST, RT, WAVES, MODE, HAS_M0, HALF, false>;

@@ -113,10 +113,13 @@ def test_ragged_valu(torch_gpu, orc, monkeypatch, prec, d):
 
 
 @pytest.mark.parametrize("prec", ["fp16", "bf16"])
-def test_half_inputs_are_exact_in_fp32(torch_gpu, orc, prec):
+@pytest.mark.parametrize("d", [2, 16, 64])
+def test_half_inputs_are_exact_in_fp32(torch_gpu, orc, prec, d):
     """fp16/bf16 products are exact in fp32, so against the oracle on the
-    rounded inputs the error is fp32 accumulation only."""
-    p = synth.random_problem(3000, 64, 40, 11, seed=77, clusters=5)
+    rounded inputs the error is fp32 accumulation only.  At d <= 16 the bias
+    seeds the accumulators through a bf16 MFMA of its three-part split, which
+    must be exact too."""
+    p = synth.random_problem(3000, d, 40, 11, seed=77 + d, clusters=5)
     Vg, X64 = to_gpu(torch_gpu, p.X, prec)
     got = gpu_eval(torch_gpu, Vg, p.sets)
     want = orc.eval(X64, p.sets, 8)
