@@ -650,28 +650,36 @@ __global__ __launch_bounds__(WAVES * 64, PERSIST ? 2 : 1) void eval_mfma_kernel(
             }
         };
         if constexpr (PAIR) {
-            // One fold site per iteration, so the running max stays in one
-            // set of registers (with two sites the compiler copies it back
-            // every iteration): two members of the same set group when this
-            // stage holds both, else the lone member folded with itself.
+            // Pairs of members of the same set group in an inner loop with
+            // one fold site, so the running max stays in one set of
+            // registers (with a pair site and a single site in one loop the
+            // compiler copies it back every iteration); a lone member (odd k,
+            // stage end) is folded outside that loop.
             int tt = 0;
             while (tt < tn) {
-                const bool two = tt + 1 < tn && p + 1 < ktile;
-                acc_t x[RT][NB], y[RT][NB];
-                chain(tile_at(tt), tile_at(tt + 1), bq, bias, x);
-                if (two) {
+                while (tt + 1 < tn && p + 1 < ktile) {
+                    acc_t x[RT][NB], y[RT][NB];
+                    chain(tile_at(tt), tile_at(tt + 1), bq, bias, x);
                     chain(tile_at(tt + 1), tile_at(tt + 2), bq, bias, y);
-                } else {
-#pragma unroll
-                    for (int rt = 0; rt < RT; ++rt) y[rt][0] = x[rt][0];
+                    fold2(x, y);
+                    tt += 2;
+                    p += 2;
+                    if (p == ktile) {
+                        group_end();
+                        p = 0;
+                        ++g;
+                    }
                 }
-                fold2(x, y);
-                tt += two ? 2 : 1;
-                p += two ? 2 : 1;
-                if (p == ktile) {
-                    group_end();
-                    p = 0;
-                    ++g;
+                if (tt < tn) {
+                    acc_t x[RT][NB];
+                    chain(tile_at(tt), tile_at(tt + 1), bq, bias, x);
+                    fold(x);
+                    tt += 1;
+                    if (++p == ktile) {
+                        group_end();
+                        p = 0;
+                        ++g;
+                    }
                 }
             }
         } else {
