@@ -141,18 +141,21 @@ def cpu_baseline(p: synth.Problem, X64: np.ndarray, budget_s: float):
     }
 
 
-# Files that define the evaluation kernels and their launch geometry (host
-# glue such as host.cpp, and the greedy kernels, do not change what the
-# traffic counters of eval_mfma_kernel / eval_valu_kernel read).
-KERNEL_FILES = ["device.hpp", "internal.h", "kernels_aux.hip", "kernels_mfma.hip", "kernels_mfma_bf16.hip",
-                "kernels_mfma_f16.hip", "kernels_mfma_f32.hip", "mfma_kernels.hpp", "../build.py"]
+# Files that define each evaluation kernel and its launch geometry (host
+# glue such as host.cpp, the second pass and the greedy kernels do not change
+# what the traffic counters of the kernel read).
+KERNEL_FILES = {
+    "eval_mfma_kernel": ["device.hpp", "internal.h", "kernels_mfma.hip", "kernels_mfma_bf16.hip",
+                         "kernels_mfma_f16.hip", "kernels_mfma_f32.hip", "mfma_kernels.hpp", "../build.py"],
+    "eval_valu_kernel": ["device.hpp", "internal.h", "kernels_aux.hip", "../build.py"],
+}
 
 
-def kernel_source_hash() -> str:
-    """Hash of everything that defines the compiled kernels (sources, build flags)."""
+def kernel_source_hash(kernel: str = "eval_mfma_kernel") -> str:
+    """Hash of everything that defines the compiled kernel (sources, build flags)."""
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2101_08763_amd", "csrc")
-    for f in KERNEL_FILES:
+    for f in KERNEL_FILES[kernel]:
         with open(os.path.join(csrc, f), "rb") as fh:
             h.update(f.encode())
             h.update(fh.read())
@@ -170,7 +173,7 @@ def load_traffic(kernel: str, workload: str):
     if not os.path.exists(path):
         return None
     t = json.load(open(path))
-    if t.get("source_sha256") != kernel_source_hash():
+    if t.get("source_sha256") != kernel_source_hash(kernel):
         return None
     return t["hbm_bytes_per_launch"]
 
@@ -199,7 +202,7 @@ def traffic_summary(d: str, kernel: str, workload: str) -> dict:
     ff = COPY_PROBE_BYTES / (cfetch_kib * 1024)
     wf = COPY_PROBE_BYTES / (cwrite_kib * 1024)
     out = {
-        "kernel": kernel, "workload": workload, "source_sha256": kernel_source_hash(),
+        "kernel": kernel, "workload": workload, "source_sha256": kernel_source_hash(kernel),
         "fetch_kib_per_dispatch": fetch_kib, "write_kib_per_dispatch": write_kib,
         "copy_probe_bytes": COPY_PROBE_BYTES, "copy_fetch_kib": cfetch_kib, "copy_write_kib": cwrite_kib,
         "fetch_scale": ff, "write_scale": wf,

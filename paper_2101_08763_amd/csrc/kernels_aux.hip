@@ -179,10 +179,25 @@ __global__ __launch_bounds__(RJ * RQ) void reduce_sets_kernel(const float *__res
     const int jl = tid % RJ, q = tid / RJ;
     const int64_t j = (int64_t)blockIdx.x * RJ + jl;
 
+    // Invalid member indices make the set's result NaN.  Checked by the
+    // threads of row q = 0 before the partial sums are read, so the two
+    // rounds of loads overlap.
+    bool bad = false;
+    if (q == 0 && j < l) {
+        for (int64_t p = 0; p < kset; ++p) {
+            const int64_t idx = sets[j * kset + p];
+            bad |= idx != kEmptySlot && (idx < 0 || idx >= n);
+        }
+        for (int64_t p = 0; p < kcommon; ++p) {
+            const int64_t idx = common[p];
+            bad |= idx != kEmptySlot && (idx < 0 || idx >= n);
+        }
+    }
+
     // Loads are issued UNR at a time (rows past G re-read row G-1 and are
     // then replaced by +0.0, which changes no sum), so the additions still
     // run in row order.
-    constexpr int UNR = 8;
+    constexpr int UNR = 16;
     double acc = 0.0;
     if (j < l) {
         for (int64_t g = q; g < G; g += RQ * UNR) {
@@ -204,15 +219,6 @@ __global__ __launch_bounds__(RJ * RQ) void reduce_sets_kernel(const float *__res
         __syncthreads();
     }
     if (q != 0 || j >= l) return;
-    bool bad = false;
-    for (int64_t p = 0; p < kset; ++p) {
-        const int64_t idx = sets[j * kset + p];
-        bad |= idx != kEmptySlot && (idx < 0 || idx >= n);
-    }
-    for (int64_t p = 0; p < kcommon; ++p) {
-        const int64_t idx = common[p];
-        bad |= idx != kEmptySlot && (idx < 0 || idx >= n);
-    }
     out[j] = bad ? __builtin_nanf("") : (float)(2.0 * part[0][jl] / (double)n);
 }
 
