@@ -38,17 +38,21 @@
 
 namespace exemcl {
 
-// 32x32x16 fp16/bf16 tiles of at most EXEMCL_SPLAT_MAX_NKB k-blocks seed
-// their accumulators with the bias by one bf16 MFMA (see eval_mfma_kernel);
-// their header holds each column's bias as three bf16 parts.
+// 32-column tiles (fp32 32x32x2, fp16/bf16 32x32x16) of at most
+// EXEMCL_SPLAT_MAX_NKB k-blocks seed their accumulators with the bias by one
+// bf16 MFMA (see eval_mfma_kernel); their header holds each column's bias as
+// three bf16 parts.
 #ifndef EXEMCL_SPLAT_MFMA
 #define EXEMCL_SPLAT_MFMA 1
 #endif
 #ifndef EXEMCL_SPLAT_MAX_NKB
 #define EXEMCL_SPLAT_MAX_NKB 4
 #endif
+#ifndef EXEMCL_SPLAT_F32
+#define EXEMCL_SPLAT_F32 1
+#endif
 constexpr bool splat_bias(int elem_bytes, int tile, int nkb) {
-    return EXEMCL_SPLAT_MFMA && elem_bytes == 2 && tile == 32 && nkb <= EXEMCL_SPLAT_MAX_NKB;
+    return EXEMCL_SPLAT_MFMA && (elem_bytes == 2 || EXEMCL_SPLAT_F32) && tile == 32 && nkb <= EXEMCL_SPLAT_MAX_NKB;
 }
 
 // Largest finite bf16 (0x7F7F).
@@ -142,7 +146,7 @@ __global__ __launch_bounds__(64) void pack_tiles_kernel(const T *__restrict__ V,
         for (int off = M::TM; off < 64; off <<= 1) sq += __shfl_xor(sq, off);
         const float b = valid ? -0.5f * sq : -FLT_MAX;
         if (grp == 0) {
-            if (sizeof(T) == 2 && splat) {
+            if (splat) {
                 // Exact three-way split: hi is b rounded to bf16, mid the
                 // rest rounded again, lo what is left (8 bits at most), so
                 // hi + mid + lo == b.  Clamped to a finite value first, so a
@@ -345,12 +349,14 @@ __global__ __launch_bounds__(WAVES * 64, PERSIST ? 2 : 1) void eval_mfma_kernel(
     // (512 bytes each) follow the NFF whole ones and bypass the prefetch ring.
     constexpr int NFF = HALF ? (NKB - 1) * NB : NF;
     constexpr int NT = WAVES * 64;
-    // Short 32x32x16 fp16/bf16 tiles are bound by VALU work, much of it the
-    // 16-register bias splat that seeds each tile's accumulators.  There
+    // On short 32-column tiles the 16-register bias splat that seeds each
+    // tile's accumulators is a large share of the VALU work (fp16/bf16: the
+    // busiest unit; fp32: its MFMA does not overlap VALU work).  There
     // (SPLAT) the header holds every column's bias as three bf16 parts and
     // one bf16 MFMA of a ones operand (coordinates 0-2 of the lanes of
     // K-group 0, zero elsewhere) against them builds the splat exactly on
-    // the matrix cores; the VALU only folds.
+    // the matrix cores, in the 32x32 accumulator layout all these shapes
+    // share; the VALU only folds.
     constexpr bool SPLAT = splat_bias((int)sizeof(T), TILE, NKB);
     constexpr int NBIAS = SPLAT ? 2 : NB;  // bias registers per tile (SPLAT: the 8 header bytes)
     constexpr int HDR = hdr_bytes(TM, NB, SPLAT);
@@ -368,7 +374,7 @@ __global__ __launch_bounds__(WAVES * 64, PERSIST ? 2 : 1) void eval_mfma_kernel(
     // divides NF; the next tile then finds fragment i in slot i.
     constexpr int PF = SCHED ? prefetch_depth(NF, EXEMCL_PF_SCHED) : (NFF < EXEMCL_PF ? NFF : EXEMCL_PF);
     static_assert(!SCHED || NF % PF == 0, "cross-tile prefetch ring must wrap at the tile end");
-    static_assert(!SPLAT || (!SCHED && NB == 1 && !HALF && MODE == MODE_SUM && !HAS_M0), "splat tiles");
+    static_assert(!SPLAT || (!SCHED && NB == 1 && !HALF), "splat tiles");
     static_assert(MODE == MODE_SUM || NB == 1, "the row-max mode stages one member per tile");
     // Pairs of tiles per fold (not for HAS_M0: the scoring of S u {c} has
     // single-member sets, where every tile is a set group of its own).
