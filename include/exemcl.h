@@ -19,9 +19,13 @@
  *   - `stream` is a hipStream_t (NULL = the null stream).  Calls are
  *     asynchronous: they validate on the host, queue kernels on `stream` and
  *     return without synchronising.  Temporary device memory comes from a
- *     library-owned stream-ordered pool and is released in stream order
- *     before the call returns.  Nothing persists between calls except that
- *     pool.  Calls on different streams may run concurrently.
+ *     library-owned stream-ordered pool; the blocks a call used are kept for
+ *     the next calls on the same stream (up to 4 per stream, for the 8 most
+ *     recently used streams), so repeated calls allocate nothing.  Kept
+ *     blocks are released when those limits are exceeded or when an
+ *     allocation fails (after waiting for the device), never while a call
+ *     uses them.  Calls on different streams may run concurrently; calls on
+ *     one stream from several host threads are safe.
  *   - V is dense row-major n x d (row stride d elements, no padding), with
  *     element type fp32, fp16 or bf16 as selected by `precision`.  Results are
  *     fp32.  Arithmetic is fp32 (fp16/bf16 products are exact in fp32).

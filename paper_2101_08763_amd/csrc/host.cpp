@@ -147,11 +147,73 @@ hipError_t get_pool(hipMemPool_t *pool) {
     return hipSuccess;
 }
 
+// Temporary blocks kept for later calls on the same stream, keyed by
+// (device, stream handle): a call takes the smallest free kept block that is
+// large enough and gives it back when it has queued its work, so repeated
+// calls allocate and free nothing.  Stream order makes the reuse safe: the
+// next call on that stream runs after the work of the previous one.  A
+// block a call is using is marked busy, so calls that share a stream from
+// different host threads never share a block.  At most kKeepPerStream
+// blocks per stream (the smallest free one is released, in stream order, to
+// make room) and kKeepStreams streams (the least recently used stream's
+// free blocks are released with hipFree, which waits for the device) are
+// kept; a failed allocation releases every free kept block and retries.
+constexpr size_t kKeepPerStream = 4;
+constexpr size_t kKeepStreams = 8;
+struct KeptBlock {
+    void *p;
+    size_t bytes;
+    bool busy;
+};
+struct StreamBlocks {
+    int dev;
+    uintptr_t sid;
+    uint64_t used;  // last-use tick
+    std::vector<KeptBlock> blocks;
+};
+std::mutex g_keep_mu;
+std::vector<StreamBlocks> g_keep;
+uint64_t g_keep_tick = 0;
+
+StreamBlocks *kept_for(int dev, uintptr_t sid) {
+    for (auto &e : g_keep)
+        if (e.dev == dev && e.sid == sid) return &e;
+    return nullptr;
+}
+
+// Releases the free blocks of entry i after waiting for the device, so it
+// is safe whatever the state of that entry's stream; drops the entry when
+// empty.
+void release_free_blocks(size_t i) {
+    (void)hipDeviceSynchronize();
+    auto &bl = g_keep[i].blocks;
+    for (size_t b = 0; b < bl.size();) {
+        if (!bl[b].busy) {
+            (void)hipFree(bl[b].p);
+            bl.erase(bl.begin() + (std::ptrdiff_t)b);
+        } else {
+            ++b;
+        }
+    }
+    if (bl.empty()) g_keep.erase(g_keep.begin() + (std::ptrdiff_t)i);
+}
+
 struct Scratch {
     void *ptr = nullptr;
     hipStream_t st = nullptr;
+    bool kept = false;
+    int dev = 0;
+    uintptr_t sid = 0;
     ~Scratch() {
-        if (ptr) hipFreeAsync(ptr, st);
+        if (!ptr) return;
+        if (!kept) {
+            hipFreeAsync(ptr, st);
+            return;
+        }
+        std::lock_guard<std::mutex> lk(g_keep_mu);
+        if (StreamBlocks *e = kept_for(dev, sid))
+            for (auto &b : e->blocks)
+                if (b.p == ptr) b.busy = false;
     }
 };
 
@@ -159,9 +221,41 @@ int alloc_scratch(Scratch *s, int64_t bytes, hipStream_t st) {
     s->st = st;
     if (bytes <= 0) return EXEMCL_OK;
     if (bytes > workspace_limit()) return EXEMCL_ENOMEM;
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) {
+        (void)hipGetLastError();
+        return EXEMCL_EDEVICE;
+    }
+    const uintptr_t sid = (uintptr_t)st;
+    s->dev = dev;
+    s->sid = sid;
+    {
+        std::lock_guard<std::mutex> lk(g_keep_mu);
+        if (StreamBlocks *e = kept_for(dev, sid)) {
+            e->used = ++g_keep_tick;
+            KeptBlock *best = nullptr;
+            for (auto &b : e->blocks)
+                if (!b.busy && b.bytes >= (size_t)bytes && (!best || b.bytes < best->bytes)) best = &b;
+            if (best) {
+                best->busy = true;
+                s->ptr = best->p;
+                s->kept = true;
+                return EXEMCL_OK;
+            }
+        }
+    }
     hipMemPool_t pool;
     if (get_pool(&pool) != hipSuccess) return EXEMCL_EDEVICE;
     hipError_t e = hipMallocFromPoolAsync(&s->ptr, (size_t)bytes, pool, st);
+    if (e == hipErrorOutOfMemory) {
+        (void)hipGetLastError();
+        {
+            std::lock_guard<std::mutex> lk(g_keep_mu);
+            for (size_t i = g_keep.size(); i-- > 0;)
+                if (g_keep[i].dev == dev) release_free_blocks(i);
+        }
+        e = hipMallocFromPoolAsync(&s->ptr, (size_t)bytes, pool, st);
+    }
     if (e == hipErrorOutOfMemory) {
         (void)hipGetLastError();
         s->ptr = nullptr;
@@ -171,6 +265,32 @@ int alloc_scratch(Scratch *s, int64_t bytes, hipStream_t st) {
         s->ptr = nullptr;
         return EXEMCL_EDEVICE;
     }
+    // Keep the new block for this stream.
+    std::lock_guard<std::mutex> lk(g_keep_mu);
+    StreamBlocks *entry = kept_for(dev, sid);
+    if (!entry) {
+        if (g_keep.size() >= kKeepStreams) {
+            size_t lru = 0;
+            for (size_t i = 1; i < g_keep.size(); ++i)
+                if (g_keep[i].used < g_keep[lru].used) lru = i;
+            release_free_blocks(lru);
+        }
+        if (g_keep.size() >= kKeepStreams) return EXEMCL_OK;  // all busy: free this block after the call
+        g_keep.push_back(StreamBlocks{dev, sid, ++g_keep_tick, {}});
+        entry = &g_keep.back();
+    }
+    auto &bl = entry->blocks;
+    if (bl.size() >= kKeepPerStream) {
+        // release the smallest free block of this stream, in stream order
+        size_t victim = bl.size();
+        for (size_t b = 0; b < bl.size(); ++b)
+            if (!bl[b].busy && (victim == bl.size() || bl[b].bytes < bl[victim].bytes)) victim = b;
+        if (victim == bl.size()) return EXEMCL_OK;  // all busy: free this block after the call
+        hipFreeAsync(bl[victim].p, st);
+        bl.erase(bl.begin() + (std::ptrdiff_t)victim);
+    }
+    bl.push_back(KeptBlock{s->ptr, (size_t)bytes, true});
+    s->kept = true;
     return EXEMCL_OK;
 }
 

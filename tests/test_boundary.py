@@ -173,3 +173,18 @@ def test_prof_enable_arguments(lib):
     assert ms.value == 0.0 and cnt.value == 0
     with pytest.raises(api.ExemclError):
         api.exemplar_prof_enable(-2)
+
+
+def test_library_needs_no_newer_hip_runtime():
+    """The library is loaded next to PyTorch's own HIP runtime (ROCm 7.0 in
+    this image), which can be older than the toolkit it is built with: every
+    versioned HIP symbol it imports must come from HIP 7.0 or earlier."""
+    import shutil
+    import subprocess
+    objdump = shutil.which("objdump")
+    if objdump is None:
+        pytest.skip("objdump not available")
+    txt = subprocess.run([objdump, "-T", api.LIB_PATH], capture_output=True, text=True, check=True).stdout
+    versions = {tuple(int(x) for x in m.split(".")) for m in re.findall(r"\bhip_(\d+\.\d+)\b", txt)}
+    assert versions, "no versioned HIP imports found"
+    assert max(versions) <= (7, 0), sorted(versions)
