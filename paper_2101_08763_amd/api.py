@@ -87,9 +87,16 @@ def precision_of(dtype) -> int:
 
 
 def _stream(stream):
+    """The HIP stream handle of `stream`, or of the current stream of the
+    current device (PyTorch's raw-stream query when it has one: it skips
+    building a Stream object, a few microseconds per call)."""
     import torch
-    s = stream if stream is not None else torch.cuda.current_stream()
-    return ctypes.c_void_p(s.cuda_stream)
+    if stream is not None:
+        return ctypes.c_void_p(stream.cuda_stream)
+    raw = getattr(torch._C, "_cuda_getCurrentRawStream", None)
+    if raw is not None:
+        return ctypes.c_void_p(raw(torch.cuda.current_device()))
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
 
 
 def _check_device(*tensors):

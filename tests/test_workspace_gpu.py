@@ -119,3 +119,17 @@ def test_gain_after_eval_on_one_stream(torch_gpu):
     for _ in range(3):
         assert np.array_equal(api.exemplar_gain(Vg, S, C).cpu().numpy(), g0)
         assert np.array_equal(gpu_eval(torch, Vg, p.sets), e0)
+
+
+def test_default_stream_is_the_current_one(torch_gpu):
+    """Without `stream=`, calls queue on PyTorch's current stream."""
+    torch = torch_gpu
+    st = torch.cuda.Stream()
+    assert (api._stream(None).value or 0) == torch.cuda.current_stream().cuda_stream
+    with torch.cuda.stream(st):
+        assert (api._stream(None).value or 0) == st.cuda_stream
+        probs = problems(torch, 1, 1100)
+        Vg, s = probs[0]
+        o = api.exemplar_eval(Vg, s)
+    st.synchronize()
+    assert np.array_equal(o.cpu().numpy(), alone(torch, probs)[0])
