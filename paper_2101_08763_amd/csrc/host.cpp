@@ -512,17 +512,33 @@ void copy_rows(void *dst, int64_t ld, const void *src, int64_t d, int64_t rows, 
     for (auto &x : th) x.join();
 }
 
+// Copy stream and events of the streamed path, created once per device and
+// kept (guarded by g_stream_mu, which serialises streamed calls).
 struct StreamedState {
     hipStream_t cs = nullptr;
     hipEvent_t copied[2] = {nullptr, nullptr}, freed[2] = {nullptr, nullptr};
-    ~StreamedState() {
-        for (int i = 0; i < 2; ++i) {
-            if (copied[i]) hipEventDestroy(copied[i]);
-            if (freed[i]) hipEventDestroy(freed[i]);
-        }
-        if (cs) hipStreamDestroy(cs);
-    }
 };
+StreamedState g_streamed[64];
+
+hipError_t streamed_state(StreamedState **out) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
+    StreamedState &ss = g_streamed[dev];
+    if (!ss.cs) {
+        hipStream_t cs = nullptr;
+        e = hipStreamCreateWithFlags(&cs, hipStreamNonBlocking);
+        for (int i = 0; i < 2 && e == hipSuccess; ++i) {
+            e = hipEventCreateWithFlags(&ss.copied[i], hipEventDisableTiming);
+            if (e == hipSuccess) e = hipEventCreateWithFlags(&ss.freed[i], hipEventDisableTiming);
+        }
+        if (e != hipSuccess) return e;
+        ss.cs = cs;
+    }
+    *out = &ss;
+    return hipSuccess;
+}
 
 int run_streamed(const void *V, int64_t n, int64_t d, const int32_t *sets, int64_t l, int64_t k, int precision,
                  int64_t rows_per_block, float *out, hipStream_t st) {
@@ -561,6 +577,51 @@ int run_streamed(const void *V, int64_t n, int64_t d, const int32_t *sets, int64
             if (pinned_reserve(&g_pin_rows[i], (size_t)(R * ld * es)) != hipSuccess) return EXEMCL_ENOMEM;
     }
 
+    Scratch ws;
+    int rc = alloc_scratch(&ws, bytes, st);
+    if (rc) return rc;
+    char *base = (char *)ws.ptr;
+    void *drows[2] = {base, base + off_rows1};
+    void *dexem = base + off_exem;
+    int32_t *didx = (int32_t *)(base + off_idx);
+    double *acc = (double *)(base + off_acc);
+    uint8_t *dbad = (uint8_t *)(base + off_bad);
+    float *dout = (float *)(base + off_out);
+    char *work = base + off_work;
+    float *partials = (float *)(work + L.off_partials);
+    void *tiles = work + L.off_tiles;
+
+    StreamedState *ss = nullptr;
+    if (streamed_state(&ss) != hipSuccess) return EXEMCL_EDEVICE;
+    // The copy stream writes the row buffers only after the work already
+    // queued on `st` (which may still use this temporary memory).
+    hipError_t e = hipEventRecord(ss->freed[0], st);
+    if (e == hipSuccess) e = hipEventRecord(ss->freed[1], st);
+
+    // Row block b into device buffer b % 2 on the copy stream, once the
+    // kernels of block b - 2 have released it.
+    const int64_t nblocks = (n + R - 1) / R;
+    auto issue_copy = [&](int64_t b) -> hipError_t {
+        const int i = (int)(b & 1);
+        const int64_t r0 = b * R, rows = std::min(R, n - r0);
+        const void *src = (const char *)V + r0 * d * es;
+        if (!direct) {
+            // The pinned buffer of block b - 2 must have reached the device.
+            if (b >= 2) {
+                const hipError_t es1 = hipEventSynchronize(ss->copied[i]);
+                if (es1 != hipSuccess) return es1;
+            }
+            copy_rows(g_pin_rows[i].p, ld, src, d, rows, es);
+            src = g_pin_rows[i].p;
+        }
+        hipError_t ec = hipStreamWaitEvent(ss->cs, ss->freed[i], 0);
+        if (ec == hipSuccess) ec = hipMemcpyAsync(drows[i], src, (size_t)(rows * ld * es), hipMemcpyHostToDevice, ss->cs);
+        if (ec == hipSuccess) ec = hipEventRecord(ss->copied[i], ss->cs);
+        return ec;
+    };
+    // The first two blocks travel while the host gathers the exemplars.
+    for (int64_t b = 0; b < std::min<int64_t>(2, nblocks) && e == hipSuccess; ++b) e = issue_copy(b);
+
     // Host side of the gather: exemplar rows (zero-padded to ld), indices
     // remapped into the compact matrix, and the sets with an invalid index.
     char *E = (char *)g_pin_exem.p;
@@ -597,51 +658,14 @@ int run_streamed(const void *V, int64_t n, int64_t d, const int32_t *sets, int64
         }
     }
 
-    Scratch ws;
-    int rc = alloc_scratch(&ws, bytes, st);
-    if (rc) return rc;
-    char *base = (char *)ws.ptr;
-    void *drows[2] = {base, base + off_rows1};
-    void *dexem = base + off_exem;
-    int32_t *didx = (int32_t *)(base + off_idx);
-    double *acc = (double *)(base + off_acc);
-    uint8_t *dbad = (uint8_t *)(base + off_bad);
-    float *dout = (float *)(base + off_out);
-    char *work = base + off_work;
-    float *partials = (float *)(work + L.off_partials);
-    void *tiles = work + L.off_tiles;
-
-    StreamedState ss;
-    if (hipStreamCreateWithFlags(&ss.cs, hipStreamNonBlocking) != hipSuccess) return EXEMCL_EDEVICE;
-    for (int i = 0; i < 2; ++i)
-        if (hipEventCreateWithFlags(&ss.copied[i], hipEventDisableTiming) != hipSuccess ||
-            hipEventCreateWithFlags(&ss.freed[i], hipEventDisableTiming) != hipSuccess)
-            return EXEMCL_EDEVICE;
-
-    hipError_t e = hipMemcpyAsync(dexem, E, (size_t)(ne * ld * es), hipMemcpyHostToDevice, st);
+    if (e == hipSuccess) e = hipMemcpyAsync(dexem, E, (size_t)(ne * ld * es), hipMemcpyHostToDevice, st);
     if (e == hipSuccess) e = hipMemcpyAsync(didx, ridx, (size_t)(ne * 4), hipMemcpyHostToDevice, st);
     if (e == hipSuccess) e = hipMemcpyAsync(dbad, bad, (size_t)l, hipMemcpyHostToDevice, st);
     if (e == hipSuccess) e = launch_pack(precision, mp, dexem, std::max<int64_t>(ne, 1), (int)ld, didx, l, k, tiles, st);
-    // The copy stream may not overwrite a row buffer before the exemplar
-    // upload and tile staging queued above are ordered before it.
-    if (e == hipSuccess) e = hipEventRecord(ss.freed[0], st);
-    if (e == hipSuccess) e = hipEventRecord(ss.freed[1], st);
-    const int64_t nblocks = (n + R - 1) / R;
     for (int64_t b = 0; b < nblocks && e == hipSuccess; ++b) {
         const int i = (int)(b & 1);
-        const int64_t r0 = b * R, rows = std::min(R, n - r0);
-        const void *src = (const char *)V + r0 * d * es;
-        if (!direct) {
-            // The pinned buffer of block b - 2 must have reached the device.
-            if (b >= 2) e = hipEventSynchronize(ss.copied[i]);
-            if (e != hipSuccess) break;
-            copy_rows(g_pin_rows[i].p, ld, src, d, rows, es);
-            src = g_pin_rows[i].p;
-        }
-        e = hipStreamWaitEvent(ss.cs, ss.freed[i], 0);
-        if (e == hipSuccess) e = hipMemcpyAsync(drows[i], src, (size_t)(rows * ld * es), hipMemcpyHostToDevice, ss.cs);
-        if (e == hipSuccess) e = hipEventRecord(ss.copied[i], ss.cs);
-        if (e == hipSuccess) e = hipStreamWaitEvent(st, ss.copied[i], 0);
+        const int64_t rows = std::min(R, n - b * R);
+        e = hipStreamWaitEvent(st, ss->copied[i], 0);
         Layout Lb;
         if (e == hipSuccess && !layout_eval(rows, d, l, k, precision, EXEMCL_PATH_MFMA, &Lb)) e = hipErrorInvalidValue;
         if (e == hipSuccess) {
@@ -651,13 +675,14 @@ int run_streamed(const void *V, int64_t n, int64_t d, const int32_t *sets, int64
             pr.end();
         }
         if (e == hipSuccess) e = launch_accum(partials, Lb.G, Lb.lpad, l, b == 0, acc, st);
-        if (e == hipSuccess) e = hipEventRecord(ss.freed[i], st);
+        if (e == hipSuccess) e = hipEventRecord(ss->freed[i], st);
+        if (e == hipSuccess && b + 2 < nblocks) e = issue_copy(b + 2);
     }
     if (e == hipSuccess) e = launch_finish(acc, dbad, l, n, dout, st);
     if (e == hipSuccess) e = hipMemcpyAsync(out, dout, (size_t)(l * 4), hipMemcpyDeviceToHost, st);
     const hipError_t es2 = hipStreamSynchronize(st);
     if (e == hipSuccess) e = es2;
-    (void)hipStreamSynchronize(ss.cs);
+    (void)hipStreamSynchronize(ss->cs);
     return status_of(e);
 }
 

@@ -294,23 +294,48 @@ hipError_t launch_zero(float *out, int64_t count, hipStream_t st) {
 // ---------------------------------------------------------------------------
 // Out-of-core evaluation: the per-set sums of one block of ground points are
 // added to an fp64 accumulator (acc[j] = sum over blocks in order, each block
-// summed over its partial rows in order), and the accumulator is turned into
-// f(S_j) = (2/n) * acc[j] at the end (NaN for a set with an invalid index).
+// summed over its partial rows in the fixed order of the second pass: row
+// lanes q, q + RQ, ... then a pairwise tree), and the accumulator is turned
+// into f(S_j) = (2/n) * acc[j] at the end (NaN for a set with an invalid
+// index).
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void accum_sets_kernel(const float *__restrict__ partials, int64_t G, int64_t lpad,
-                                                          int64_t l, int first, double *__restrict__ acc) {
-    const int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x;
-    if (j >= l) return;
+__global__ __launch_bounds__(RJ * RQ) void accum_sets_kernel(const float *__restrict__ partials, int64_t G,
+                                                             int64_t lpad, int64_t l, int first,
+                                                             double *__restrict__ acc) {
+    __shared__ double part[RQ][RJ];
+    const int tid = threadIdx.x;
+    const int jl = tid % RJ, q = tid / RJ;
+    const int64_t j = (int64_t)blockIdx.x * RJ + jl;
+    constexpr int UNR = 16;
     double s = 0.0;
-    for (int64_t g = 0; g < G; ++g) s += (double)partials[g * lpad + j];
-    acc[j] = first ? s : acc[j] + s;
+    if (j < l) {
+        for (int64_t g = q; g < G; g += RQ * UNR) {
+            float x[UNR];
+#pragma unroll
+            for (int u = 0; u < UNR; ++u) x[u] = partials[min(g + u * RQ, G - 1) * lpad + j];
+#pragma unroll
+            for (int u = 0; u < UNR; ++u)
+                if (g + u * RQ >= G) x[u] = 0.0f;
+#pragma unroll
+            for (int u = 0; u < UNR; ++u) s += (double)x[u];
+        }
+    }
+    part[q][jl] = s;
+    __syncthreads();
+#pragma unroll
+    for (int w = RQ / 2; w >= 1; w >>= 1) {
+        if (q < w) part[q][jl] += part[q + w][jl];
+        __syncthreads();
+    }
+    if (q != 0 || j >= l) return;
+    acc[j] = first ? part[0][jl] : acc[j] + part[0][jl];
 }
 
 hipError_t launch_accum(const float *partials, int64_t G, int64_t lpad, int64_t l, bool first, double *acc,
                         hipStream_t st) {
     if (l == 0) return hipSuccess;
-    hipLaunchKernelGGL(accum_sets_kernel, dim3((unsigned)((l + 255) / 256)), dim3(256), 0, st, partials, G, lpad, l,
-                       first ? 1 : 0, acc);
+    hipLaunchKernelGGL(accum_sets_kernel, dim3((unsigned)((l + RJ - 1) / RJ)), dim3(RJ * RQ), 0, st, partials, G,
+                       lpad, l, first ? 1 : 0, acc);
     return hipGetLastError();
 }
 
