@@ -332,6 +332,10 @@ int g_prof_every = 0;    // record every g_prof_every-th call; 0 = off
 int64_t g_prof_calls = 0;  // calls seen since recording was switched on
 std::vector<std::pair<hipEvent_t, hipEvent_t>> g_prof_events;
 
+// Timing of one sampled call's dominant kernel.  For the MFMA kernel the
+// pair is handed to the launch (hipExtLaunchKernel), whose dispatch records
+// it at the kernel's start and end; for other launches record() brackets
+// them on the stream.
 struct ProfRange {
     hipEvent_t a = nullptr, b = nullptr;
     hipStream_t st;
@@ -345,13 +349,17 @@ struct ProfRange {
         if (hipEventCreate(&a) != hipSuccess || hipEventCreate(&b) != hipSuccess) {
             if (a) hipEventDestroy(a);
             a = b = nullptr;
-            return;
         }
-        hipEventRecord(a, st);
     }
+    void record_start() {
+        if (a) hipEventRecord(a, st);
+    }
+    void record_stop() {
+        if (b) hipEventRecord(b, st);
+    }
+    // Keep the pair for exemplar_prof_read (after a successful launch).
     void end() {
         if (!a) return;
-        hipEventRecord(b, st);
         std::lock_guard<std::mutex> lk(g_prof_mu);
         g_prof_events.emplace_back(a, b);
         a = b = nullptr;
@@ -375,13 +383,15 @@ hipError_t run_chunk(const Layout &L, char *base, const void *V, int64_t n, int6
         if (e == hipSuccess) {
             ProfRange pr(st);
             e = launch_mfma(precision, MODE_SUM, L.mp, rows->V, n, (int)rows->ld, tiles, mfma_tiles_per_group(L.mp, k),
-                            L.ngroups, L.gpc, m0, partials, L.lpad, nullptr, st);
-            pr.end();
+                            L.ngroups, L.gpc, m0, partials, L.lpad, nullptr, st, pr.a, pr.b);
+            if (e == hipSuccess) pr.end();
         }
     } else if (L.path == EXEMCL_PATH_VALU) {
         ProfRange pr(st);
+        pr.record_start();
         e = launch_valu(precision, L.vp, V, n, (int)d, sets, l, k, partials, L.lpad, st);
-        pr.end();
+        pr.record_stop();
+        if (e == hipSuccess) pr.end();
     }
     if (e == hipSuccess)
         e = launch_reduce(partials, L.G, L.lpad, l, n, sets, k, common, kcommon, out, st);
@@ -671,8 +681,8 @@ int run_streamed(const void *V, int64_t n, int64_t d, const int32_t *sets, int64
         if (e == hipSuccess) {
             ProfRange pr(st);
             e = launch_mfma(precision, MODE_SUM, mp, drows[i], rows, (int)ld, tiles, mfma_tiles_per_group(mp, k),
-                            Lb.ngroups, Lb.gpc, nullptr, partials, Lb.lpad, nullptr, st);
-            pr.end();
+                            Lb.ngroups, Lb.gpc, nullptr, partials, Lb.lpad, nullptr, st, pr.a, pr.b);
+            if (e == hipSuccess) pr.end();
         }
         if (e == hipSuccess) e = launch_accum(partials, Lb.G, Lb.lpad, l, b == 0, acc, st);
         if (e == hipSuccess) e = hipEventRecord(ss->freed[i], st);

@@ -41,6 +41,9 @@ struct MfmaArgs {
     float *partials;
     int64_t lpad;
     float *rowmax;
+    // Optional: events the kernel's dispatch itself records at its start and
+    // end (hipExtLaunchKernel), so their interval is the kernel's run time.
+    hipEvent_t ev_start = nullptr, ev_stop = nullptr;
 };
 
 // Per-storage-type instantiations (kernels_mfma_{f32,f16,bf16}.hip).
@@ -97,7 +100,8 @@ enum Mode { MODE_SUM = 0, MODE_ROWMAX = 1 };
 // columns); rowmax must not alias m0.
 hipError_t launch_mfma(int prec, int mode, const MfmaPlan &pl, const void *V, int64_t n, int ld,
                        const void *tiles, int64_t kt, int64_t ngroups, int64_t groups_per_chunk,
-                       const float *m0, float *partials, int64_t lpad, float *rowmax, hipStream_t st);
+                       const float *m0, float *partials, int64_t lpad, float *rowmax, hipStream_t st,
+                       hipEvent_t ev_start = nullptr, hipEvent_t ev_stop = nullptr);
 
 hipError_t launch_valu(int prec, const ValuPlan &pl, const void *V, int64_t n, int d, const int32_t *sets,
                        int64_t l, int64_t k, float *partials, int64_t lpad, hipStream_t st);

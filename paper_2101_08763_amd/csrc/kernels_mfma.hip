@@ -98,8 +98,8 @@ hipError_t launch_pack(int prec, const MfmaPlan &pl, const void *V, int64_t n, i
 
 hipError_t launch_mfma(int prec, int mode, const MfmaPlan &pl, const void *V, int64_t n, int ld, const void *tiles,
                        int64_t kt, int64_t ngroups, int64_t gpc, const float *m0, float *partials, int64_t lpad,
-                       float *rowmax, hipStream_t st) {
-    const MfmaArgs x{V, n, ld, tiles, kt, ngroups, gpc, m0, partials, lpad, rowmax};
+                       float *rowmax, hipStream_t st, hipEvent_t ev_start, hipEvent_t ev_stop) {
+    const MfmaArgs x{V, n, ld, tiles, kt, ngroups, gpc, m0, partials, lpad, rowmax, ev_start, ev_stop};
     switch (prec) {
     case P_FP32: return eval_run_f32(pl, mode, x, st);
     case P_FP16: return mode == MODE_SUM ? eval_run_f16(pl, mode, x, st) : hipErrorInvalidValue;

@@ -33,6 +33,8 @@
 #include <float.h>
 #include <stdlib.h>
 
+#include <hip/hip_ext.h>
+
 #include "device.hpp"
 #include "internal.h"
 
@@ -847,13 +849,13 @@ hipError_t eval_launch_t(const MfmaArgs &x, hipStream_t st) {
         else use_persist = slots > 0 && np == 1 && nq == 1 && G * x.ngroups >= 8 * slots;
     }
     if (use_persist) {
-        hipLaunchKernelGGL(kernp, dim3((unsigned)slots, 1), dim3(WAVES * 64), lds, st, (const T *)x.V, x.n, x.ld,
-                           (const unsigned char *)x.tiles, x.kt, x.ngroups, x.gpc, G, x.m0, x.partials, x.lpad,
-                           x.rowmax);
+        hipExtLaunchKernelGGL(kernp, dim3((unsigned)slots, 1), dim3(WAVES * 64), lds, st, x.ev_start, x.ev_stop, 0,
+                              (const T *)x.V, x.n, x.ld, (const unsigned char *)x.tiles, x.kt, x.ngroups, x.gpc, G,
+                              x.m0, x.partials, x.lpad, x.rowmax);
     } else {
-        hipLaunchKernelGGL(kern, dim3((unsigned)G, (unsigned)chunks), dim3(WAVES * 64), lds, st, (const T *)x.V, x.n,
-                           x.ld, (const unsigned char *)x.tiles, x.kt, x.ngroups, x.gpc, G, x.m0, x.partials, x.lpad,
-                           x.rowmax);
+        hipExtLaunchKernelGGL(kern, dim3((unsigned)G, (unsigned)chunks), dim3(WAVES * 64), lds, st, x.ev_start,
+                              x.ev_stop, 0, (const T *)x.V, x.n, x.ld, (const unsigned char *)x.tiles, x.kt,
+                              x.ngroups, x.gpc, G, x.m0, x.partials, x.lpad, x.rowmax);
     }
     return hipGetLastError();
 }
