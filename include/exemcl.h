@@ -233,13 +233,15 @@ EXEMCL_API int exemplar_plan(int64_t n, int64_t d, int64_t l, int64_t k, int pre
 /*
  * Profiling hook.  exemplar_prof_enable(N), N >= 1, makes every N-th
  * following exemplar_eval / exemplar_gain call (the first one included)
- * record a pair of HIP events on its stream around its dominant kernel (the
- * contraction + epilogue kernel); exemplar_prof_enable(0) stops recording;
+ * time its dominant kernel (the contraction + epilogue kernel) with a pair
+ * of HIP events: for the MFMA kernel the kernel's dispatch records them at
+ * its start and end, for the VALU kernel they are recorded around it on the
+ * stream.  exemplar_prof_enable(0) stops recording;
  * N < 0 is EXEMCL_EINVAL.  exemplar_prof_read waits for the recorded events,
  * writes the summed kernel time in milliseconds and the number of recorded
  * launches, and forgets them.  Either pointer may be NULL.  Meant for
- * benchmarks: each recorded call costs two event records on the stream,
- * which also delay the kernels after them, so long runs sample (N > 1).
+ * benchmarks: each recorded call costs two events, so long runs sample
+ * (N > 1).
  */
 EXEMCL_API int exemplar_prof_enable(int every);
 EXEMCL_API int exemplar_prof_read(double *ms_total, int64_t *launches);
