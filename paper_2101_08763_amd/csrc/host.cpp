@@ -270,10 +270,12 @@ int alloc_scratch(Scratch *s, int64_t bytes, hipStream_t st) {
     StreamBlocks *entry = kept_for(dev, sid);
     if (!entry) {
         if (g_keep.size() >= kKeepStreams) {
-            size_t lru = 0;
-            for (size_t i = 1; i < g_keep.size(); ++i)
-                if (g_keep[i].used < g_keep[lru].used) lru = i;
-            release_free_blocks(lru);
+            // the least recently used stream of this device (the device wait
+            // in release_free_blocks covers the current device only)
+            size_t lru = g_keep.size();
+            for (size_t i = 0; i < g_keep.size(); ++i)
+                if (g_keep[i].dev == dev && (lru == g_keep.size() || g_keep[i].used < g_keep[lru].used)) lru = i;
+            if (lru < g_keep.size()) release_free_blocks(lru);
         }
         if (g_keep.size() >= kKeepStreams) return EXEMCL_OK;  // all busy: free this block after the call
         g_keep.push_back(StreamBlocks{dev, sid, ++g_keep_tick, {}});
