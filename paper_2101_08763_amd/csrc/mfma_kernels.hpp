@@ -515,8 +515,8 @@ __global__ __launch_bounds__(WAVES * 64, PERSIST ? 2 : 1) void eval_mfma_kernel(
     }
     const bf16x8 ones = __builtin_bit_cast(bf16x8, ones_w);
     auto chain = [&](const unsigned char *tb, const unsigned char *tnext, vec_t (&bq)[PF], float (&bias)[NBIAS],
-                     acc_t (&acc)[RT][NB]) {
-        if constexpr (!SCHED) head(tb, bq, bias);
+                     acc_t (&acc)[RT][NB], bool read_head = true) {
+        if (!SCHED && read_head) head(tb, bq, bias);
         const vec_t *B = reinterpret_cast<const vec_t *>(tb + HDR);
         const vec_t *Bn = reinterpret_cast<const vec_t *>(tnext + HDR);
         if constexpr (SPLAT) {
@@ -657,7 +657,48 @@ __global__ __launch_bounds__(WAVES * 64, PERSIST ? 2 : 1) void eval_mfma_kernel(
                     for (int i = 0; i < M::ACC; ++i) m[rt][i] = m_init(rt, i);
             }
         };
-        if constexpr (PAIR) {
+        if constexpr (PAIR && NKB == 1) {
+            // Tiles of one k-block hold a few MFMAs each: the operands of the
+            // next pair are read from LDS while this pair is folded (a
+            // scheduling barrier keeps the reads there), instead of right
+            // before their use.  Otherwise as below.
+            vec_t bqa[PF], bqb[PF];
+            float ba[NBIAS], bbb[NBIAS];
+            int tt = 0;
+            head(tile_at(0), bqa, ba);
+            head(tile_at(1), bqb, bbb);
+            while (tt < tn) {
+                while (tt + 1 < tn && p + 1 < ktile) {
+                    acc_t x[RT][NB], y[RT][NB];
+                    chain(tile_at(tt), tile_at(tt + 1), bqa, ba, x, false);
+                    chain(tile_at(tt + 1), tile_at(tt + 2), bqb, bbb, y, false);
+                    head(tile_at(tt + 2), bqa, ba);
+                    head(tile_at(tt + 3), bqb, bbb);
+                    __builtin_amdgcn_sched_barrier(0);
+                    fold2(x, y);
+                    tt += 2;
+                    p += 2;
+                    if (p == ktile) {
+                        group_end();
+                        p = 0;
+                        ++g;
+                    }
+                }
+                if (tt < tn) {
+                    acc_t x[RT][NB];
+                    chain(tile_at(tt), tile_at(tt + 1), bqa, ba, x, false);
+                    fold(x);
+                    tt += 1;
+                    if (++p == ktile) {
+                        group_end();
+                        p = 0;
+                        ++g;
+                    }
+                    head(tile_at(tt), bqa, ba);
+                    head(tile_at(tt + 1), bqb, bbb);
+                }
+            }
+        } else if constexpr (PAIR) {
             // Pairs of members of the same set group in an inner loop with
             // one fold site, so the running max stays in one set of
             // registers (with a pair site and a single site in one loop the
