@@ -309,12 +309,20 @@ struct MfmaRows {
     Scratch copy;
 };
 
+// The single-k-block fp32 layout reads rows one coordinate at a time and
+// takes V as it is.
+bool rows_as_is(int precision, int64_t d) {
+    MfmaPlan mp;
+    return mfma_plan(precision, d, &mp) && mp.il;
+}
+
 int64_t pad_bytes(int precision, int64_t n, int64_t d) {
+    if (rows_as_is(precision, d)) return 0;
     return (d * elem_size(precision)) % 16 == 0 ? 0 : align_up(n * mfma_row_stride(precision, d) * elem_size(precision), 256);
 }
 
 int prepare_rows(const void *V, int64_t n, int64_t d, int precision, hipStream_t st, MfmaRows *r) {
-    if (mfma_rows_ready(precision, V, d)) {
+    if (rows_as_is(precision, d) || mfma_rows_ready(precision, V, d)) {
         r->V = V;
         r->ld = d;
         return EXEMCL_OK;

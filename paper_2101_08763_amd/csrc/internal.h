@@ -25,7 +25,8 @@ struct MfmaPlan {
     int kb_dims;    // coordinates per k-block
     int nb;         // set members per staged tile (a set group spans ceil(k / nb) tiles)
     int half;       // 1: the last k-block holds 16 coordinates (16x16x16 instruction)
-    int splat;      // 1: tile headers hold bf16 bias parts for the splat MFMA (32x32x16, few k-blocks)
+    int splat;      // 1: tile headers hold bf16 bias parts for the splat MFMA (32-column tiles, few k-blocks)
+    int il;         // 1: fp32 single k-block with coordinates 2e + g (ceil(d/2) instructions; rows need no padding)
 };
 
 bool mfma_plan(int prec, int64_t d, MfmaPlan *p);

@@ -39,12 +39,16 @@ bool mfma_plan(int prec, int64_t d, MfmaPlan *p) {
     q.nb = 1;
     q.half = 0;
     q.splat = 0;
+    q.il = 0;
     if (prec == P_FP32 && d <= 256) {
         // v_mfma_f32_32x32x2_f32, 8 coordinates per k-block
         q.tile = 32;
         q.kb_dims = 8;
         q.nkb = bucket((int)((d + 7) / 8));
-        q.nks_last = q.nkb == 1 ? (int)(d < 4 ? d : 4) : 4;  // instruction e covers dims e and 4 + e
+        // instruction e covers dims e and 4 + e, or 2e and 2e + 1 in the
+        // single-k-block layout (il)
+        q.il = il_layout(4, 32, q.nkb) ? 1 : 0;
+        q.nks_last = q.nkb == 1 ? (q.il ? (int)((d + 1) / 2) : (int)(d < 4 ? d : 4)) : 4;
     } else if (prec == P_FP32) {
         // v_mfma_f32_16x16x4_f32, 16 coordinates per k-block
         q.tile = 16;

@@ -57,6 +57,20 @@ constexpr bool splat_bias(int elem_bytes, int tile, int nkb) {
     return EXEMCL_SPLAT_MFMA && (elem_bytes == 2 || EXEMCL_SPLAT_F32) && tile == 32 && nkb <= EXEMCL_SPLAT_MAX_NKB;
 }
 
+// fp32 tiles of one k-block (d <= 8) pair coordinates per instruction:
+// element e of lane group g holds coordinate 2e + g, so instruction e of
+// v_mfma_f32_32x32x2_f32 covers coordinates 2e and 2e + 1 and ceil(d / 2)
+// instructions cover d (the contiguous layout, e and 4 + e per instruction,
+// needs min(d, 4)).  Rows are then read one coordinate at a time, so they
+// need no 16-byte alignment or padding.
+#ifndef EXEMCL_IL
+#define EXEMCL_IL 1
+#endif
+constexpr bool il_layout(int elem_bytes, int tile, int nkb) {
+    return EXEMCL_IL && elem_bytes == 4 && tile == 32 && nkb == 1;
+}
+__device__ __forceinline__ int il_dim(int grp, int e) { return 2 * e + grp; }
+
 // Largest finite bf16 (0x7F7F).
 constexpr float kBf16Max = 3.38953139e38f;
 
@@ -94,7 +108,7 @@ constexpr int tile_bytes_of(int hdr, int nff, int nhalf) { return hdr + nff * 10
 template <typename T, int TILE>
 __global__ __launch_bounds__(64) void pack_tiles_kernel(const T *__restrict__ V, int64_t n, int ld,
                                                         const int32_t *__restrict__ sets, int64_t l,
-                                                        int64_t k, int nkb, int half, int splat,
+                                                        int64_t k, int nkb, int half, int splat, int il,
                                                         unsigned char *__restrict__ tiles) {
     using M = Mfma<T, TILE>;
     constexpr int NB = M::NB;
@@ -117,8 +131,17 @@ __global__ __launch_bounds__(64) void pack_tiles_kernel(const T *__restrict__ V,
         const int64_t r = valid ? idx : n;  // row n reads as zeros
         float sq = 0.0f;
         for (int kb = 0; kb < nfull; ++kb) {
-            const typename M::vec_t v =
-                lanevec_keep<M>(lanevec_raw<M>(V, n, ld, r, kb, grp), lanevec_live<M>(n, ld, r, kb, grp));
+            typename M::vec_t v;
+            if (sizeof(T) == 4 && il) {
+                // coordinate 2e + grp, read one at a time (rows may be unpadded)
+#pragma unroll
+                for (int e = 0; e < M::VEC; ++e) {
+                    const int c = il_dim(grp, e);
+                    v[e] = (r < n && c < ld) ? V[r * (int64_t)ld + c] : (typename M::elem_t)0.0f;
+                }
+            } else {
+                v = lanevec_keep<M>(lanevec_raw<M>(V, n, ld, r, kb, grp), lanevec_live<M>(n, ld, r, kb, grp));
+            }
             dst[(kb * NB + h) * 64 + lane] = v;
 #pragma unroll
             for (int e = 0; e < M::VEC; ++e) {
@@ -360,6 +383,7 @@ __global__ __launch_bounds__(WAVES * 64, PERSIST ? 2 : 1) void eval_mfma_kernel(
     // the matrix cores, in the 32x32 accumulator layout all these shapes
     // share; the VALU only folds.
     constexpr bool SPLAT = splat_bias((int)sizeof(T), TILE, NKB);
+    constexpr bool IL = il_layout((int)sizeof(T), TILE, NKB);
     constexpr int NBIAS = SPLAT ? 2 : NB;  // bias registers per tile (SPLAT: the 8 header bytes)
     constexpr int HDR = hdr_bytes(TM, NB, SPLAT);
     constexpr int TB = tile_bytes_of(HDR, NFF, HALF ? NB : 0);
@@ -447,10 +471,19 @@ __global__ __launch_bounds__(WAVES * 64, PERSIST ? 2 : 1) void eval_mfma_kernel(
 #pragma unroll
     for (int rt = 0; rt < RT; ++rt) {
         const int lrow = wave * RT * TM + rt * TM + lr;
+        if constexpr (IL) {
 #pragma unroll
-        for (int kb = 0; kb < NKF; ++kb) {
-            const int d0 = M::dim(kb, grp, 0);
-            a[rt][kb] = window_load16<vec_t>(vwin, d0 < ldv ? (uint32_t)((lrow * ldv + d0) * (int)sizeof(T)) : kDeadOffset);
+            for (int e = 0; e < M::VEC; ++e) {
+                const int c = il_dim(grp, e);
+                a[rt][0][e] = window_load4(vwin, c < ldv ? (uint32_t)((lrow * ldv + c) * 4) : kDeadOffset);
+            }
+        } else {
+#pragma unroll
+            for (int kb = 0; kb < NKF; ++kb) {
+                const int d0 = M::dim(kb, grp, 0);
+                a[rt][kb] =
+                    window_load16<vec_t>(vwin, d0 < ldv ? (uint32_t)((lrow * ldv + d0) * (int)sizeof(T)) : kDeadOffset);
+            }
         }
         if constexpr (HALF) {
             const int d0 = M::hdim(NKF, grp, 0);  // ld and d0 are multiples of 4: the 4 elements are in the row
@@ -831,10 +864,11 @@ hipError_t pack_launch(const MfmaPlan &pl, const void *V, int64_t n, int ld, con
                        int64_t k, void *tiles, hipStream_t st) {
     if (pl.half && !Mfma<T, TILE>::HAS_HALF) return hipErrorInvalidValue;
     if ((pl.splat != 0) != splat_bias((int)sizeof(T), TILE, pl.nkb)) return hipErrorInvalidValue;
+    if ((pl.il != 0) != il_layout((int)sizeof(T), TILE, pl.nkb)) return hipErrorInvalidValue;
     const int64_t ngroups = (l + TILE - 1) / TILE;
     const int64_t kt = (k + Mfma<T, TILE>::NB - 1) / Mfma<T, TILE>::NB;
     hipLaunchKernelGGL((pack_tiles_kernel<T, TILE>), dim3((unsigned)(ngroups * kt)), dim3(64), 0, st,
-                       (const T *)V, n, ld, sets, l, k, pl.nkb, pl.half, pl.splat, (unsigned char *)tiles);
+                       (const T *)V, n, ld, sets, l, k, pl.nkb, pl.half, pl.splat, pl.il, (unsigned char *)tiles);
     return hipGetLastError();
 }
 
