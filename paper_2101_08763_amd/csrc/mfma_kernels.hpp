@@ -336,7 +336,9 @@ __device__ __forceinline__ void wait_vmcnt() {
 // Evaluation kernel.
 //
 // grid.x = row blocks of WAVES*RT*TM consecutive points, grid.y = chunks of
-// gpc set groups.  Wavefront w owns RT row tiles of TM points.
+// gpc set groups (or, PERSIST, one workgroup per resident slot walking
+// several (row block, set group range) segments).  Wavefront w owns RT row
+// tiles of TM points, held in registers for the whole segment.
 //
 // The chunk's tiles are one contiguous byte range in global memory, streamed
 // into a ring of NBUF LDS stage buffers of SB bytes (TPS whole tiles each) by
@@ -347,7 +349,13 @@ __device__ __forceinline__ void wait_vmcnt() {
 // s+NBUF-1.
 //
 // NKS_LAST = MFMA instructions fed by the last k-block (fp32 packs KS_PER_KB
-// instructions per k-block; tiny d uses fewer).
+// instructions per k-block; tiny d uses fewer, see il_layout).
+//
+// Per tile: the accumulators start at the column's bias (a splat, or one
+// bf16 MFMA for SPLAT tiles), the MFMA chain adds <v, s>, and the running max
+// per (point, set) folds the tile in (pairs of tiles with one max3 where a
+// tile holds one member).  At a set group's end the running max is summed
+// and set back to its initial value.
 //
 // MODE_SUM: each wavefront writes its partial sum per set,
 //   partials[(rb * WAVES + w) * lpad + j] = sum over its rows of
