@@ -313,7 +313,7 @@ struct MfmaRows {
 // takes V as it is.
 bool rows_as_is(int precision, int64_t d) {
     MfmaPlan mp;
-    return mfma_plan(precision, d, &mp) && mp.il;
+    return mfma_plan(precision, d, &mp) && mp.il && mp.nkb == 1;
 }
 
 int64_t pad_bytes(int precision, int64_t n, int64_t d) {

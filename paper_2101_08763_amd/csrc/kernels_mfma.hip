@@ -45,10 +45,17 @@ bool mfma_plan(int prec, int64_t d, MfmaPlan *p) {
         q.tile = 32;
         q.kb_dims = 8;
         q.nkb = bucket((int)((d + 7) / 8));
-        // instruction e covers dims e and 4 + e, or 2e and 2e + 1 in the
-        // single-k-block layout (il)
-        q.il = il_layout(4, 32, q.nkb) ? 1 : 0;
-        q.nks_last = q.nkb == 1 ? (q.il ? (int)((d + 1) / 2) : (int)(d < 4 ? d : 4)) : 4;
+        // instruction e covers dims e and 4 + e, or 2e and 2e + 1 in a
+        // paired last k-block (il): one k-block, or an exact bucket whose
+        // last block holds r <= 4 coordinates
+        const int r = (int)(d - 8 * ((d + 7) / 8 - 1));  // coordinates in the last block, 1..8
+        if (q.nkb == 1)
+            q.nks_last = EXEMCL_IL ? (int)((d + 1) / 2) : (int)(d < 4 ? d : 4);
+        else if (q.nkb == (d + 7) / 8 && r <= 4)
+            q.nks_last = EXEMCL_IL ? (r + 1) / 2 : 4;
+        else
+            q.nks_last = 4;
+        q.il = il_layout(4, 32, q.nkb, q.nks_last) ? 1 : 0;
     } else if (prec == P_FP32) {
         // v_mfma_f32_16x16x4_f32, 16 coordinates per k-block
         q.tile = 16;

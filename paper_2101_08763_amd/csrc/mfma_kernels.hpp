@@ -57,17 +57,19 @@ constexpr bool splat_bias(int elem_bytes, int tile, int nkb) {
     return EXEMCL_SPLAT_MFMA && (elem_bytes == 2 || EXEMCL_SPLAT_F32) && tile == 32 && nkb <= EXEMCL_SPLAT_MAX_NKB;
 }
 
-// fp32 tiles of one k-block (d <= 8) pair coordinates per instruction:
-// element e of lane group g holds coordinate 2e + g, so instruction e of
-// v_mfma_f32_32x32x2_f32 covers coordinates 2e and 2e + 1 and ceil(d / 2)
-// instructions cover d (the contiguous layout, e and 4 + e per instruction,
-// needs min(d, 4)).  Rows are then read one coordinate at a time, so they
-// need no 16-byte alignment or padding.
+// fp32 32x32x2 tiles whose last k-block holds r <= 4 coordinates pair them
+// per instruction: in that k-block element e of lane group g holds
+// coordinate 2e + g, so instruction e covers coordinates 2e and 2e + 1 and
+// ceil(r / 2) instructions cover it (the contiguous layout, e and 4 + e per
+// instruction, needs all 4 once r > 2).  With a single k-block (d <= 8)
+// every row is read one coordinate at a time, so V needs no 16-byte
+// alignment or padding.  A kernel uses the paired last block when it has
+// one k-block or fewer than 4 instructions in the last one.
 #ifndef EXEMCL_IL
 #define EXEMCL_IL 1
 #endif
-constexpr bool il_layout(int elem_bytes, int tile, int nkb) {
-    return EXEMCL_IL && elem_bytes == 4 && tile == 32 && nkb == 1;
+constexpr bool il_layout(int elem_bytes, int tile, int nkb, int nks_last) {
+    return EXEMCL_IL && elem_bytes == 4 && tile == 32 && (nkb == 1 || nks_last < 4);
 }
 __device__ __forceinline__ int il_dim(int grp, int e) { return 2 * e + grp; }
 
@@ -132,11 +134,12 @@ __global__ __launch_bounds__(64) void pack_tiles_kernel(const T *__restrict__ V,
         float sq = 0.0f;
         for (int kb = 0; kb < nfull; ++kb) {
             typename M::vec_t v;
-            if (sizeof(T) == 4 && il) {
-                // coordinate 2e + grp, read one at a time (rows may be unpadded)
+            if (sizeof(T) == 4 && il && kb == nfull - 1) {
+                // last k-block: coordinate kb*8 + 2e + grp, read one at a time
+                // (single-block rows may be unpadded)
 #pragma unroll
                 for (int e = 0; e < M::VEC; ++e) {
-                    const int c = il_dim(grp, e);
+                    const int c = kb * M::KB_DIMS + il_dim(grp, e);
                     v[e] = (r < n && c < ld) ? V[r * (int64_t)ld + c] : (typename M::elem_t)0.0f;
                 }
             } else {
@@ -391,7 +394,7 @@ __global__ __launch_bounds__(WAVES * 64, PERSIST ? 2 : 1) void eval_mfma_kernel(
     // the matrix cores, in the 32x32 accumulator layout all these shapes
     // share; the VALU only folds.
     constexpr bool SPLAT = splat_bias((int)sizeof(T), TILE, NKB);
-    constexpr bool IL = il_layout((int)sizeof(T), TILE, NKB);
+    constexpr bool IL = il_layout((int)sizeof(T), TILE, NKB, NKS_LAST);
     constexpr int NBIAS = SPLAT ? 2 : NB;  // bias registers per tile (SPLAT: the 8 header bytes)
     constexpr int HDR = hdr_bytes(TM, NB, SPLAT);
     constexpr int TB = tile_bytes_of(HDR, NFF, HALF ? NB : 0);
@@ -479,15 +482,15 @@ __global__ __launch_bounds__(WAVES * 64, PERSIST ? 2 : 1) void eval_mfma_kernel(
 #pragma unroll
     for (int rt = 0; rt < RT; ++rt) {
         const int lrow = wave * RT * TM + rt * TM + lr;
-        if constexpr (IL) {
 #pragma unroll
-            for (int e = 0; e < M::VEC; ++e) {
-                const int c = il_dim(grp, e);
-                a[rt][0][e] = window_load4(vwin, c < ldv ? (uint32_t)((lrow * ldv + c) * 4) : kDeadOffset);
-            }
-        } else {
+        for (int kb = 0; kb < NKF; ++kb) {
+            if (IL && kb == NKF - 1) {
 #pragma unroll
-            for (int kb = 0; kb < NKF; ++kb) {
+                for (int e = 0; e < M::VEC; ++e) {
+                    const int c = kb * M::KB_DIMS + il_dim(grp, e);
+                    a[rt][kb][e] = window_load4(vwin, c < ldv ? (uint32_t)((lrow * ldv + c) * 4) : kDeadOffset);
+                }
+            } else {
                 const int d0 = M::dim(kb, grp, 0);
                 a[rt][kb] =
                     window_load16<vec_t>(vwin, d0 < ldv ? (uint32_t)((lrow * ldv + d0) * (int)sizeof(T)) : kDeadOffset);
@@ -872,7 +875,7 @@ hipError_t pack_launch(const MfmaPlan &pl, const void *V, int64_t n, int ld, con
                        int64_t k, void *tiles, hipStream_t st) {
     if (pl.half && !Mfma<T, TILE>::HAS_HALF) return hipErrorInvalidValue;
     if ((pl.splat != 0) != splat_bias((int)sizeof(T), TILE, pl.nkb)) return hipErrorInvalidValue;
-    if ((pl.il != 0) != il_layout((int)sizeof(T), TILE, pl.nkb)) return hipErrorInvalidValue;
+    if ((pl.il != 0) != il_layout((int)sizeof(T), TILE, pl.nkb, pl.nks_last)) return hipErrorInvalidValue;
     const int64_t ngroups = (l + TILE - 1) / TILE;
     const int64_t kt = (k + Mfma<T, TILE>::NB - 1) / Mfma<T, TILE>::NB;
     hipLaunchKernelGGL((pack_tiles_kernel<T, TILE>), dim3((unsigned)(ngroups * kt)), dim3(64), 0, st,
@@ -976,6 +979,31 @@ constexpr int waves_of() {
 }
 
 // One storage type: pick the instantiation for the plan's k-block bucket.
+// fp32 32x32x2 with more than one k-block and a paired last block of
+// KSL (1 or 2) instructions.
+template <typename T, int TILE, int MODE, int KSL>
+hipError_t eval_dispatch_last(const MfmaPlan &pl, const MfmaArgs &x, hipStream_t st) {
+    switch (pl.nkb) {
+    case 2: return eval_launch<T, TILE, 2, KSL, rt_of<T, TILE, 2>(), waves_of<T, TILE, 2>(), MODE>(x, st);
+    case 3: return eval_launch<T, TILE, 3, KSL, rt_of<T, TILE, 3>(), waves_of<T, TILE, 3>(), MODE>(x, st);
+    case 4: return eval_launch<T, TILE, 4, KSL, rt_of<T, TILE, 4>(), waves_of<T, TILE, 4>(), MODE>(x, st);
+    case 5: return eval_launch<T, TILE, 5, KSL, rt_of<T, TILE, 5>(), waves_of<T, TILE, 5>(), MODE>(x, st);
+    case 6: return eval_launch<T, TILE, 6, KSL, rt_of<T, TILE, 6>(), waves_of<T, TILE, 6>(), MODE>(x, st);
+    case 7: return eval_launch<T, TILE, 7, KSL, rt_of<T, TILE, 7>(), waves_of<T, TILE, 7>(), MODE>(x, st);
+    case 8: return eval_launch<T, TILE, 8, KSL, rt_of<T, TILE, 8>(), waves_of<T, TILE, 8>(), MODE>(x, st);
+    case 10: return eval_launch<T, TILE, 10, KSL, rt_of<T, TILE, 10>(), waves_of<T, TILE, 10>(), MODE>(x, st);
+    case 12: return eval_launch<T, TILE, 12, KSL, rt_of<T, TILE, 12>(), waves_of<T, TILE, 12>(), MODE>(x, st);
+    case 13: return eval_launch<T, TILE, 13, KSL, rt_of<T, TILE, 13>(), waves_of<T, TILE, 13>(), MODE>(x, st);
+    case 14: return eval_launch<T, TILE, 14, KSL, rt_of<T, TILE, 14>(), waves_of<T, TILE, 14>(), MODE>(x, st);
+    case 16: return eval_launch<T, TILE, 16, KSL, rt_of<T, TILE, 16>(), waves_of<T, TILE, 16>(), MODE>(x, st);
+    case 20: return eval_launch<T, TILE, 20, KSL, rt_of<T, TILE, 20>(), waves_of<T, TILE, 20>(), MODE>(x, st);
+    case 24: return eval_launch<T, TILE, 24, KSL, rt_of<T, TILE, 24>(), waves_of<T, TILE, 24>(), MODE>(x, st);
+    case 28: return eval_launch<T, TILE, 28, KSL, rt_of<T, TILE, 28>(), waves_of<T, TILE, 28>(), MODE>(x, st);
+    case 32: return eval_launch<T, TILE, 32, KSL, rt_of<T, TILE, 32>(), waves_of<T, TILE, 32>(), MODE>(x, st);
+    }
+    return hipErrorInvalidValue;
+}
+
 template <typename T, int TILE, int MODE>
 hipError_t eval_dispatch(const MfmaPlan &pl, const MfmaArgs &x, hipStream_t st) {
     if constexpr (TILE == 16 && sizeof(T) == 4) {
@@ -1014,6 +1042,12 @@ hipError_t eval_dispatch(const MfmaPlan &pl, const MfmaArgs &x, hipStream_t st) 
                 return eval_launch<T, TILE, 1, KL, rt_of<T, TILE, 1>(), waves_of<T, TILE, 1>(), MODE>(x, st);
             }
         }
+        if constexpr (KL == 4 && TILE == 32) {
+            // a last k-block of at most 4 coordinates, paired per instruction
+            if (pl.nks_last == 1) return eval_dispatch_last<T, TILE, MODE, 1>(pl, x, st);
+            if (pl.nks_last == 2) return eval_dispatch_last<T, TILE, MODE, 2>(pl, x, st);
+        }
+        if (pl.nks_last != KL) return hipErrorInvalidValue;
         switch (pl.nkb) {
         case 2: return eval_launch<T, TILE, 2, KL, rt_of<T, TILE, 2>(), waves_of<T, TILE, 2>(), MODE>(x, st);
         case 3: return eval_launch<T, TILE, 3, KL, rt_of<T, TILE, 3>(), waves_of<T, TILE, 3>(), MODE>(x, st);
