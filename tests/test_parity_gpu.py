@@ -229,6 +229,28 @@ def test_edge_cases(torch_gpu, orc):
     check(gpu_eval(torch, Lg, [[0, 1], [1, 2]]), [13 / 3, 13 / 3], 14 / 3, "fp32", "worked example")
 
 
+@pytest.mark.parametrize("prec,d", [("fp32", 2), ("fp32", 5), ("fp32", 8), ("fp32", 32), ("fp32", 100),
+                                    ("fp16", 12), ("bf16", 64)])
+def test_rows_at_any_alignment(torch_gpu, orc, prec, d):
+    """V given as a view starting one element into its storage (4- or 2-byte
+    aligned): rows read as they are (fp32, d <= 8) or through the padded
+    copy must give the same results as aligned V."""
+    torch = torch_gpu
+    n = 2001
+    p = synth.random_problem(n + 1, d, 37, 6, seed=600 + d, clusters=3)
+    Vfull, X64full = to_gpu(torch, p.X, prec)
+    Vview = Vfull.reshape(-1)[d:].reshape(n, d)     # rows 1..n, storage offset of one row
+    Vview1 = Vfull.reshape(-1)[1:1 + n * d].reshape(n, d)  # one element in: misaligned rows
+    sets = np.minimum(p.sets, n - 1).astype(np.int32)
+    X64 = X64full.reshape(-1)[1:1 + n * d].reshape(n, d)
+    got = gpu_eval(torch, Vview1, sets)
+    check(got, orc.eval(X64, sets, 8), orc.loss_e0(X64), prec, f"misaligned d={d}")
+    aligned = gpu_eval(torch, Vview1.contiguous().clone(), sets)
+    assert np.array_equal(got, aligned)
+    X64b = X64full[1:]
+    check(gpu_eval(torch, Vview, sets), orc.eval(X64b, sets, 8), orc.loss_e0(X64b), prec, f"row offset d={d}")
+
+
 def test_sqnorm(torch_gpu, orc):
     for prec in ("fp32", "fp16", "bf16"):
         p = synth.random_problem(5000, 37, 1, 1, seed=3, clusters=3)
