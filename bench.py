@@ -34,6 +34,7 @@ METRIC = "set evaluations/s and distance terms/s (n·k·l) + % of MFMA/HBM peak"
 COPY_PROBE_BYTES = 1 << 30   # plain device copy used to calibrate the HBM byte counters
 PROFILES = os.path.join(ROOT, "profiles")
 PEAK_TFLOPS = {"fp32": 157.3, "fp16": 2516.6, "bf16": 2516.6}  # dense MFMA, MI355X
+HBM_PEAK_GBS = 8000.0  # HBM3E, MI355X
 DTYPE_NAME = {"fp32": "f32", "fp16": "f16", "bf16": "bf16"}
 
 
@@ -148,6 +149,7 @@ KERNEL_FILES = {
     "eval_mfma_kernel": ["device.hpp", "internal.h", "kernels_mfma.hip", "kernels_mfma_bf16.hip",
                          "kernels_mfma_f16.hip", "kernels_mfma_f32.hip", "mfma_kernels.hpp", "../build.py"],
     "eval_valu_kernel": ["device.hpp", "internal.h", "kernels_aux.hip", "../build.py"],
+    "sqnorm_kernel": ["device.hpp", "internal.h", "kernels_aux.hip", "../build.py"],
 }
 
 
@@ -401,6 +403,72 @@ def run_greedy(args, w, dev):
     print(json.dumps(rec), flush=True)
 
 
+def run_sqnorm(args, w, dev):
+    """Squared norms q[i] = ||v_i||^2 (exemplar_sqnorm) of the workload's
+    points: one HBM-bound pass over V.  Algorithmic bytes per launch are
+    n * d * element size read plus 4 n written; a device copy of V's bytes
+    (read + write) is timed beside it as the practical ceiling.  One JSON
+    line of its own."""
+    import torch
+    log(f"generating {w.name}: {w.note}")
+    p = synth.make(w)
+    Xs, X64 = synth.rounded(p.X, w.precision)
+    V = (Xs if isinstance(Xs, torch.Tensor) else torch.from_numpy(Xs)).to(dev).contiguous()
+    q = torch.empty(w.n, dtype=torch.float32, device=dev)
+    step = lambda: api.exemplar_sqnorm(V, out=q)  # noqa: E731
+    warmup, sec = warm_up(step, args.warmup, torch.cuda.synchronize)
+    steps = timed_steps(args.steps, sec, min_steps=20)
+    stream = torch.cuda.current_stream()
+
+    def timed(fn):
+        ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        ev0.record(stream)
+        for _ in range(steps):
+            fn()
+        ev1.record(stream)
+        torch.cuda.synchronize()
+        return ev0.elapsed_time(ev1) / steps
+
+    ms = timed(step)
+    vflat = V.reshape(-1)
+    dst = torch.empty_like(vflat)
+    for _ in range(5):
+        dst.copy_(vflat)
+    copy_ms = timed(lambda: dst.copy_(vflat))
+    vbytes = V.numel() * V.element_size()
+    algo = vbytes + 4 * w.n
+    achieved = algo / (ms * 1e-3) / 1e9
+    rec = {
+        "metric": "squared norms/s (exemplar_sqnorm) + % of HBM peak",
+        "value": w.n / (ms * 1e-3), "unit": "rows/s", "ms_per_call": ms, "steps": steps, "warmup": warmup,
+        "higher_is_better": True, "dtype": DTYPE_NAME[w.precision], "data": "synthetic",
+        "config": {"workload": f"{w.name} points: {w.note}", "n": w.n, "d": w.d, "precision": w.precision},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": load_traffic("sqnorm_kernel", w.name),
+                     "kernel": "sqnorm_kernel", "bytes_per_launch": algo},
+        "device_copy": {"bytes": 2 * vbytes, "ms": copy_ms, "gb_per_s": 2 * vbytes / (copy_ms * 1e-3) / 1e9},
+    }
+    if not args.no_cpu_baseline:
+        import oracle
+        o = oracle.load()
+        rows = min(w.n, max(1, int(2e8 // max(w.d, 1))))
+        t0 = time.perf_counter()
+        reps = 0
+        while True:
+            o.sqnorm(X64[:rows])
+            reps += 1
+            dt = time.perf_counter() - t0
+            if dt >= min(args.cpu_budget, 10.0):
+                break
+        rec["cpu_baseline"] = {
+            "value": rows * reps / dt, "unit": "rows/s", "cores": 1, "kind": "oracle",
+            "sample": f"the first {rows} rows, {reps} passes (fp64, one thread) on {cpu_model()}",
+            "seconds": dt,
+        }
+    print(json.dumps(rec), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -429,6 +497,8 @@ def main():
     ap.add_argument("--rows-per-block", type=int, default=0, help="row block of --streamed (0 = library default)")
     ap.add_argument("--greedy-rounds", type=int, default=0, metavar="K",
                     help="time exemplar_greedy with K rounds over the workload's points instead (fp32)")
+    ap.add_argument("--sqnorm", action="store_true",
+                    help="time exemplar_sqnorm over the workload's points instead (HBM-bound); one JSON line")
     args = ap.parse_args()
 
     if args.traffic_summary:
@@ -457,6 +527,9 @@ def main():
     w = synth.WORKLOADS[args.workload]
     if args.greedy_rounds > 0:
         run_greedy(args, w, dev)
+        return
+    if args.sqnorm:
+        run_sqnorm(args, w, dev)
         return
     if args.streamed:
         if w.mode != "eval":

@@ -213,6 +213,10 @@ EXEMCL_API int exemplar_greedy(const float *V, int64_t n, int64_t d, int64_t K, 
  *   V, n, d, precision  as for exemplar_eval
  *   q                   device, n floats; written
  *
+ * One pass over V (HBM-bound).  The environment variable
+ * EXEMCL_SQNORM_MAX_BLOCKS=<b> lowers the number of workgroups per launch
+ * (tests: several grid passes at a small n); the results do not depend on it.
+ *
  * Errors: EINVAL / EDEVICE as above.
  */
 EXEMCL_API int exemplar_sqnorm(const void *V, int64_t n, int64_t d, int precision, float *q,

@@ -220,6 +220,8 @@ def exemplar_sqnorm(V, out=None, stream=None):
     n, d = V.shape
     if out is None:
         out = torch.empty(n, dtype=torch.float32, device=V.device)
+    elif out.dtype != torch.float32 or out.numel() != n:
+        raise ValueError("out must be float32 with n elements")
     with torch.cuda.device(_check_device(V, out)):
         rc = load().exemplar_sqnorm(_ptr(V), n, d, prec, _ptr(out), _stream(stream))
     if rc != EXEMCL_OK:

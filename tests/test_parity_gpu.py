@@ -251,14 +251,68 @@ def test_rows_at_any_alignment(torch_gpu, orc, prec, d):
     check(gpu_eval(torch, Vview, sets), orc.eval(X64b, sets, 8), orc.loss_e0(X64b), prec, f"row offset d={d}")
 
 
-def test_sqnorm(torch_gpu, orc):
-    for prec in ("fp32", "fp16", "bf16"):
-        p = synth.random_problem(5000, 37, 1, 1, seed=3, clusters=3)
-        Vg, X64 = to_gpu(torch_gpu, p.X, prec)
+SQNORM_D = [1, 2, 3, 4, 7, 8, 16, 37, 64, 100, 256, 512, 1000, 4099]
+
+
+@pytest.mark.parametrize("prec", ["fp32", "fp16", "bf16"])
+def test_sqnorm(torch_gpu, orc, prec):
+    """q = ||v||^2 (A1) over d spanning one to many lanes per row and whole or
+    ragged 16-byte groups, on aligned rows, on rows one element into their
+    storage (same order of additions, so the same bits) and at a row offset."""
+    torch = torch_gpu
+    for d in SQNORM_D:
+        n = 5003 if d <= 512 else 701
+        p = synth.random_problem(n + 1, d, 1, 1, seed=3 + d, clusters=3)
+        Vfull, X64full = to_gpu(torch, p.X, prec)
+        say(f"  sqnorm {prec} d={d} n={n}")
+        q = api.exemplar_sqnorm(Vfull[:n])
+        torch.cuda.synchronize()
+        np.testing.assert_allclose(q.cpu().numpy(), orc.sqnorm(X64full[:n]), rtol=1e-5, atol=0)
+        Vmis = Vfull.reshape(-1)[1:1 + n * d].reshape(n, d)
+        qmis = api.exemplar_sqnorm(Vmis)
+        qal = api.exemplar_sqnorm(Vmis.contiguous().clone())
+        qoff = api.exemplar_sqnorm(Vfull[1:])
+        torch.cuda.synchronize()
+        X64mis = X64full.reshape(-1)[1:1 + n * d].reshape(n, d)
+        np.testing.assert_allclose(qmis.cpu().numpy(), orc.sqnorm(X64mis), rtol=1e-5, atol=0)
+        assert np.array_equal(qmis.cpu().numpy(), qal.cpu().numpy())
+        np.testing.assert_allclose(qoff.cpu().numpy(), orc.sqnorm(X64full[1:]), rtol=1e-5, atol=0)
+
+
+@pytest.mark.parametrize("prec,d", [("fp32", 1), ("fp32", 33), ("fp16", 64), ("bf16", 512)])
+def test_sqnorm_several_passes(torch_gpu, orc, monkeypatch, prec, d):
+    """A grid capped at a few workgroups (EXEMCL_SQNORM_MAX_BLOCKS) walks
+    the rows in several passes: same bits as one pass, oracle within
+    tolerance."""
+    torch = torch_gpu
+    n = 40_009 if d <= 64 else 5_003
+    rng = np.random.default_rng(77 + d)
+    Vg, X64 = to_gpu(torch, synth.points(rng, n, d, 0), prec)
+    one = api.exemplar_sqnorm(Vg)
+    torch.cuda.synchronize()
+    for cap in ("1", "7"):
+        monkeypatch.setenv("EXEMCL_SQNORM_MAX_BLOCKS", cap)
+        say(f"  sqnorm {prec} n={n} d={d} max blocks {cap}")
         q = api.exemplar_sqnorm(Vg)
-        torch_gpu.cuda.synchronize()
-        want = orc.sqnorm(X64)
-        np.testing.assert_allclose(q.cpu().numpy(), want, rtol=1e-5, atol=0)
+        torch.cuda.synchronize()
+        assert np.array_equal(q.cpu().numpy(), one.cpu().numpy())
+    np.testing.assert_allclose(one.cpu().numpy(), orc.sqnorm(X64), rtol=1e-5, atol=0)
+
+
+def test_sqnorm_large(torch_gpu, orc):
+    """The points of the 1 000 000 x 256 fp16 workload (the one the squared
+    norm benchmark times): rows sampled over the whole range against the
+    oracle."""
+    torch = torch_gpu
+    p = synth.make("large1m")
+    Vg, _ = to_gpu(torch, p.X, "fp16")
+    n = p.X.shape[0]
+    say(f"  sqnorm large1m n={n}")
+    q = api.exemplar_sqnorm(Vg)
+    torch.cuda.synchronize()
+    idx = np.unique(np.concatenate([np.arange(100), np.random.default_rng(5).integers(0, n, 3000), [n - 1]]))
+    _, X64 = synth.rounded(p.X[idx], "fp16")
+    np.testing.assert_allclose(q.cpu().numpy()[idx], orc.sqnorm(X64), rtol=1e-5, atol=0)
 
 
 # ---------------------------------------------------------------------------
