@@ -25,7 +25,10 @@
  *     blocks are released when those limits are exceeded or when an
  *     allocation fails (after waiting for the device), never while a call
  *     uses them.  Calls on different streams may run concurrently; calls on
- *     one stream from several host threads are safe.
+ *     one stream from several host threads are safe.  Kept blocks are keyed
+ *     by the stream's handle, and a new stream can get the handle of a
+ *     destroyed one: synchronise a stream before destroying it while calls
+ *     of this library are still queued on it.
  *   - V is dense row-major n x d (row stride d elements, no padding), with
  *     element type fp32, fp16 or bf16 as selected by `precision`.  Results are
  *     fp32.  Arithmetic is fp32 (fp16/bf16 products are exact in fp32).

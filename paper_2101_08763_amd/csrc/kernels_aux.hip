@@ -393,7 +393,7 @@ __global__ __launch_bounds__(256) void sqnorm_kernel(const T *__restrict__ V, in
             row[u] = V + (i < n ? i : n - 1) * (int64_t)d;
             s[u] = 0.0f;
         }
-        for (int t0 = j * G; t0 < d; t0 += L * G) {
+        for (int64_t t0 = (int64_t)j * G; t0 < d; t0 += (int64_t)L * G) {  // 64-bit: d may be near INT32_MAX
             vec_t v[U];
 #pragma unroll
             for (int u = 0; u < U; ++u) {

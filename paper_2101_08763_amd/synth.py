@@ -58,8 +58,9 @@ WORKLOADS = {
     "large1m": Workload("large1m", 1_000_000, 256, 2048, 32, 100, 4, "fp16", "eval",
                         "1 000 000 points, d=256, 100-Gaussian mixture, fp16; 2048 sets of 32"),
 }
+# The d/precision sweep; bf16 storage is measured beside the fp16 lines.
 for _d in (2, 16, 128, 512):
-    for _p in ("fp32", "fp16"):
+    for _p in ("fp32", "fp16", "bf16"):
         _w = Workload(f"sweep_d{_d}_{_p}", 100_000, _d, 1024, 16, 0, 3, _p, "eval",
                       f"100 000 points, d={_d}, i.i.d. N(0,1), {_p}; 1024 sets of 16")
         WORKLOADS[_w.name] = _w
