@@ -145,7 +145,7 @@ def test_mix50k_all_sets(torch_gpu, orc):
 
 
 @pytest.mark.parametrize("d", [2, 16, 128, 512])
-@pytest.mark.parametrize("prec", ["fp32", "fp16"])
+@pytest.mark.parametrize("prec", ["fp32", "fp16", "bf16"])
 def test_sweep_sampled(torch_gpu, orc, d, prec):
     p = synth.make(f"sweep_d{d}_{prec}")
     say(f"sweep d={d} {prec}: 100 000 points, 1024 sets of 16")
