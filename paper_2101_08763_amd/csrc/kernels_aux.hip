@@ -167,10 +167,20 @@ hipError_t launch_valu(int prec, const ValuPlan &pl, const void *V, int64_t n, i
 // are then added by a fixed pairwise tree.  The order depends on G only, so
 // the result of a set does not depend on the batch it is in.  The index
 // check turns a set with an index outside [0, n) other than the empty slot
-// into NaN.
+// into NaN: row lane q checks members q, q + RQ, ... and a failed check makes
+// its lane sum NaN, which the tree carries to the result.
 // ---------------------------------------------------------------------------
-constexpr int RJ = 16;
-constexpr int RQ = 64;
+#ifndef EXEMCL_RED_RJ
+#define EXEMCL_RED_RJ 16
+#endif
+#ifndef EXEMCL_RED_RQ
+#define EXEMCL_RED_RQ 64
+#endif
+constexpr int RJ = EXEMCL_RED_RJ;
+constexpr int RQ = EXEMCL_RED_RQ;
+static_assert((RQ & (RQ - 1)) == 0 && RJ * RQ <= 1024, "RQ a power of two, at most 1024 threads");
+
+__device__ inline bool bad_index(int64_t idx, int64_t n) { return idx != kEmptySlot && (idx < 0 || idx >= n); }
 
 __global__ __launch_bounds__(RJ * RQ) void reduce_sets_kernel(const float *__restrict__ partials, int64_t G,
                                                               int64_t lpad, int64_t l, int64_t n,
@@ -182,20 +192,13 @@ __global__ __launch_bounds__(RJ * RQ) void reduce_sets_kernel(const float *__res
     const int jl = tid % RJ, q = tid / RJ;
     const int64_t j = (int64_t)blockIdx.x * RJ + jl;
 
-    // Invalid member indices make the set's result NaN.  Checked by the
-    // threads of row q = 0 before the partial sums are read, so the two
-    // rounds of loads overlap.
-    bool bad = false;
-    if (q == 0 && j < l) {
-        for (int64_t p = 0; p < kset; ++p) {
-            const int64_t idx = sets[j * kset + p];
-            bad |= idx != kEmptySlot && (idx < 0 || idx >= n);
-        }
-        for (int64_t p = 0; p < kcommon; ++p) {
-            const int64_t idx = common[p];
-            bad |= idx != kEmptySlot && (idx < 0 || idx >= n);
-        }
-    }
+    // The first member of each row lane's share is loaded before the
+    // partial sums (from an address clamped into the arrays, without a
+    // branch) and checked after them, so the loads overlap.  kset >= 1 and
+    // l >= 1 whenever this kernel runs; when common is empty, sets[0] is read
+    // in its place and ignored.
+    const int32_t i0 = sets[(j < l ? j : l - 1) * kset + (q < kset ? q : kset - 1)];
+    const int32_t c0 = *(kcommon > 0 ? common + (q < kcommon ? q : kcommon - 1) : sets);
 
     // Loads are issued UNR at a time (rows past G re-read row G-1 and are
     // then replaced by +0.0, which changes no sum), so the additions still
@@ -214,7 +217,13 @@ __global__ __launch_bounds__(RJ * RQ) void reduce_sets_kernel(const float *__res
             for (int u = 0; u < UNR; ++u) acc += (double)x[u];
         }
     }
-    part[q][jl] = acc;
+    bool bad = false;
+    if (j < l) {
+        bad = (q < kset && bad_index(i0, n)) || (q < kcommon && bad_index(c0, n));
+        for (int64_t p = q + RQ; p < kset; p += RQ) bad |= bad_index(sets[j * kset + p], n);
+        for (int64_t p = q + RQ; p < kcommon; p += RQ) bad |= bad_index(common[p], n);
+    }
+    part[q][jl] = bad ? __builtin_nan("") : acc;
     __syncthreads();
 #pragma unroll
     for (int w = RQ / 2; w >= 1; w >>= 1) {
@@ -222,7 +231,7 @@ __global__ __launch_bounds__(RJ * RQ) void reduce_sets_kernel(const float *__res
         __syncthreads();
     }
     if (q != 0 || j >= l) return;
-    out[j] = bad ? __builtin_nanf("") : (float)(2.0 * part[0][jl] / (double)n);
+    out[j] = (float)(2.0 * part[0][jl] / (double)n);
 }
 
 hipError_t launch_reduce(const float *partials, int64_t G, int64_t lpad, int64_t l, int64_t n,
