@@ -142,25 +142,31 @@ def cpu_baseline(p: synth.Problem, X64: np.ndarray, budget_s: float):
     }
 
 
-# Files that define each evaluation kernel and its launch geometry (host
-# glue such as host.cpp, the second pass and the greedy kernels do not change
-# what the traffic counters of the kernel read).
+# Files that define each kernel and its launch geometry (host glue such as
+# host.cpp, the second pass and the greedy kernels do not change what the
+# traffic counters of the kernel read); the compiler flags are hashed too.
 KERNEL_FILES = {
     "eval_mfma_kernel": ["device.hpp", "internal.h", "kernels_mfma.hip", "kernels_mfma_bf16.hip",
-                         "kernels_mfma_f16.hip", "kernels_mfma_f32.hip", "mfma_kernels.hpp", "../build.py"],
-    "eval_valu_kernel": ["device.hpp", "internal.h", "kernels_aux.hip", "../build.py"],
-    "sqnorm_kernel": ["device.hpp", "internal.h", "kernels_aux.hip", "../build.py"],
+                         "kernels_mfma_f16.hip", "kernels_mfma_f32.hip", "mfma_kernels.hpp"],
+    "eval_valu_kernel": ["device.hpp", "internal.h", "kernels_aux.hip"],
+    "sqnorm_kernel": ["device.hpp", "internal.h", "kernels_sqnorm.hip"],
 }
 
 
 def kernel_source_hash(kernel: str = "eval_mfma_kernel") -> str:
-    """Hash of everything that defines the compiled kernel (sources, build flags)."""
+    """Hash of everything that defines the compiled kernel: its sources and
+    the compiler flags (without the machine-dependent include paths)."""
+    from paper_2101_08763_amd import build as B
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2101_08763_amd", "csrc")
     for f in KERNEL_FILES[kernel]:
         with open(os.path.join(csrc, f), "rb") as fh:
             h.update(f.encode())
             h.update(fh.read())
+    flags = [x for x in B.FLAGS if not x.startswith("-I")]
+    if kernel == "eval_mfma_kernel":
+        flags += B.MFMA_FLAGS
+    h.update(" ".join([B.ARCH] + flags).encode())
     return h.hexdigest()
 
 
