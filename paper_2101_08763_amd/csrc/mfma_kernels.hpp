@@ -124,26 +124,59 @@ __global__ __launch_bounds__(64) void pack_tiles_kernel(const T *__restrict__ V,
     const int nfull = nkb - half;  // whole k-blocks; a half one follows when half = 1
     unsigned char *tile = tiles + t * (int64_t)tile_bytes_of(HDR, nfull * NB, half * NB);
     typename M::vec_t *dst = reinterpret_cast<typename M::vec_t *>(tile + HDR);
+    // Member indices of every column group first, from addresses clamped
+    // into the set matrix (l, k >= 1 whenever this kernel runs), so their
+    // loads overlap.
+    int32_t raw[NB];
 #pragma unroll
     for (int h = 0; h < NB; ++h) {
         const int64_t p = q * NB + h;
-        int64_t idx = -1;
-        if (j < l && p < k) idx = sets[j * k + p];
+        raw[h] = sets[(j < l ? j : l - 1) * k + (p < k ? p : k - 1)];
+    }
+#pragma unroll
+    for (int h = 0; h < NB; ++h) {
+        const int64_t p = q * NB + h;
+        const int64_t idx = (j < l && p < k) ? (int64_t)raw[h] : -1;
         const bool valid = idx >= 0 && idx < n;
         const int64_t r = valid ? idx : n;  // row n reads as zeros
         float sq = 0.0f;
-        for (int kb = 0; kb < nfull; ++kb) {
-            typename M::vec_t v;
-            if (sizeof(T) == 4 && il && kb == nfull - 1) {
-                // last k-block: coordinate kb*8 + 2e + grp, read one at a time
-                // (single-block rows may be unpadded)
+        // Up to KBATCH k-blocks are loaded before any is stored, so the loads
+        // overlap (indices past the last block re-read it and are not
+        // stored); ||s||^2 still runs over k-blocks and elements in order.
+        // A paired last k-block (fp32) follows the others.
+        const bool paired = sizeof(T) == 4 && il;
+        const int nreg = paired ? nfull - 1 : nfull;
+        constexpr int KBATCH = 8;
+        for (int kb0 = 0; kb0 < nreg; kb0 += KBATCH) {
+            typename M::vec_t vb[KBATCH];
 #pragma unroll
-                for (int e = 0; e < M::VEC; ++e) {
-                    const int c = kb * M::KB_DIMS + il_dim(grp, e);
-                    v[e] = (r < n && c < ld) ? V[r * (int64_t)ld + c] : (typename M::elem_t)0.0f;
+            for (int u = 0; u < KBATCH; ++u) {
+                const int kb = kb0 + u < nreg ? kb0 + u : nreg - 1;
+                vb[u] = lanevec_raw<M>(V, n, ld, r, kb, grp);
+            }
+#pragma unroll
+            for (int u = 0; u < KBATCH; ++u) {
+                const int kb = kb0 + u;
+                if (kb < nreg) {
+                    const typename M::vec_t v = lanevec_keep<M>(vb[u], lanevec_live<M>(n, ld, r, kb, grp));
+                    dst[(kb * NB + h) * 64 + lane] = v;
+#pragma unroll
+                    for (int e = 0; e < M::VEC; ++e) {
+                        const float x = to_f32(v[e]);
+                        sq = fmaf(x, x, sq);
+                    }
                 }
-            } else {
-                v = lanevec_keep<M>(lanevec_raw<M>(V, n, ld, r, kb, grp), lanevec_live<M>(n, ld, r, kb, grp));
+            }
+        }
+        if (paired) {
+            // last k-block: coordinate kb*8 + 2e + grp, read one at a time
+            // (single-block rows may be unpadded)
+            const int kb = nfull - 1;
+            typename M::vec_t v;
+#pragma unroll
+            for (int e = 0; e < M::VEC; ++e) {
+                const int c = kb * M::KB_DIMS + il_dim(grp, e);
+                v[e] = (r < n && c < ld) ? V[r * (int64_t)ld + c] : (typename M::elem_t)0.0f;
             }
             dst[(kb * NB + h) * 64 + lane] = v;
 #pragma unroll
@@ -876,6 +909,7 @@ hipError_t pack_launch(const MfmaPlan &pl, const void *V, int64_t n, int ld, con
     if (pl.half && !Mfma<T, TILE>::HAS_HALF) return hipErrorInvalidValue;
     if ((pl.splat != 0) != splat_bias((int)sizeof(T), TILE, pl.nkb)) return hipErrorInvalidValue;
     if ((pl.il != 0) != il_layout((int)sizeof(T), TILE, pl.nkb, pl.nks_last)) return hipErrorInvalidValue;
+    if (l < 1 || k < 1) return hipErrorInvalidValue;  // the kernel reads sets[0] at least
     const int64_t ngroups = (l + TILE - 1) / TILE;
     const int64_t kt = (k + Mfma<T, TILE>::NB - 1) / Mfma<T, TILE>::NB;
     hipLaunchKernelGGL((pack_tiles_kernel<T, TILE>), dim3((unsigned)(ngroups * kt)), dim3(64), 0, st,
