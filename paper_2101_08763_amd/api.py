@@ -115,6 +115,16 @@ def _check_device(*tensors):
     return dev
 
 
+def _device_scope(dev):
+    """Make `dev` current for the call; a no-op (no device switch) when it
+    already is, which saves the switch and restore on every call."""
+    import contextlib
+    import torch
+    if dev is None or dev.index == torch.cuda.current_device():
+        return contextlib.nullcontext()
+    return torch.cuda.device(dev)
+
+
 def _ptr(t):
     return ctypes.c_void_p(t.data_ptr()) if t is not None and t.numel() > 0 else ctypes.c_void_p(0)
 
@@ -133,7 +143,7 @@ def exemplar_eval(V, sets, out=None, stream=None):
         out = torch.empty(l, dtype=torch.float32, device=V.device)
     elif out.dtype != torch.float32 or out.numel() != l:
         raise ValueError("out must be float32 with l elements")
-    with torch.cuda.device(_check_device(V, sets, out)):
+    with _device_scope(_check_device(V, sets, out)):
         rc = load().exemplar_eval(_ptr(V), n, d, _ptr(sets), l, k, prec, _ptr(out), _stream(stream))
     if rc != EXEMCL_OK:
         raise ExemclError(rc, "exemplar_eval")
@@ -181,7 +191,7 @@ def exemplar_gain(V, S, cands, out=None, stream=None):
     l = cands.numel()
     if out is None:
         out = torch.empty(l, dtype=torch.float32, device=V.device)
-    with torch.cuda.device(_check_device(V, S if S.numel() else None, cands, out)):
+    with _device_scope(_check_device(V, S if S.numel() else None, cands, out)):
         rc = load().exemplar_gain(_ptr(V), n, d, _ptr(S), S.numel(), _ptr(cands), l, _ptr(out),
                                   _stream(stream))
     if rc != EXEMCL_OK:
@@ -206,7 +216,7 @@ def exemplar_greedy(V, K, S_out=None, f_out=None, stream=None):
         f_out = torch.empty(max(K, 0), dtype=torch.float32, device=V.device)
     if S_out.dtype != torch.int32 or f_out.dtype != torch.float32 or S_out.numel() < K or f_out.numel() < K:
         raise ValueError("S_out must be int32 and f_out float32, with K elements each")
-    with torch.cuda.device(_check_device(V, S_out if K > 0 else None, f_out if K > 0 else None)):
+    with _device_scope(_check_device(V, S_out if K > 0 else None, f_out if K > 0 else None)):
         rc = load().exemplar_greedy(_ptr(V), n, d, K, _ptr(S_out), _ptr(f_out), _stream(stream))
     if rc != EXEMCL_OK:
         raise ExemclError(rc, "exemplar_greedy")
@@ -222,7 +232,7 @@ def exemplar_sqnorm(V, out=None, stream=None):
         out = torch.empty(n, dtype=torch.float32, device=V.device)
     elif out.dtype != torch.float32 or out.numel() != n:
         raise ValueError("out must be float32 with n elements")
-    with torch.cuda.device(_check_device(V, out)):
+    with _device_scope(_check_device(V, out)):
         rc = load().exemplar_sqnorm(_ptr(V), n, d, prec, _ptr(out), _stream(stream))
     if rc != EXEMCL_OK:
         raise ExemclError(rc, "exemplar_sqnorm")
