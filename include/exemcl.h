@@ -232,6 +232,11 @@ EXEMCL_API int exemplar_sqnorm(const void *V, int64_t n, int64_t d, int precisio
  * may be NULL).  The path depends on (d, k, precision) only, never on l or n,
  * which is what keeps out[j] independent of the batch.  The environment
  * variable EXEMCL_PATH=valu|mfma forces a path where it applies (tests).
+ * Two more variables tune the MFMA launch without changing any result:
+ * EXEMCL_PERSIST=0|2 forces the plain or the persistent grid (default: a
+ * rule on the kernel's occupancy and the work per resident workgroup), and
+ * EXEMCL_WG_TARGET=<n> sets how many workgroups a launch aims for when set
+ * groups are chunked.  All variables are read on every call.
  * Returns EINVAL for arguments exemplar_eval would reject, else EXEMCL_OK.
  */
 EXEMCL_API int exemplar_plan(int64_t n, int64_t d, int64_t l, int64_t k, int precision, int *path,

@@ -1,5 +1,5 @@
 """Persistent and plain-grid launches of the MFMA evaluation kernel give the
-same bits.
+same bits, and so does any grouping of set groups into chunks.
 
 Every (row block, set group) unit is computed by exactly one workgroup, in
 the same order, whichever launch runs it, and each wavefront writes its own
@@ -93,3 +93,18 @@ def test_gain_persistent_equals_plain(torch_gpu, orc, monkeypatch):
     plain, pers = both_launches(monkeypatch, run)
     assert np.array_equal(plain, pers)
     check(pers[:4], orc.gain(X64, S, cands[:4], 8), orc.loss_e0(X64), "fp32", "persistent gain vs oracle")
+
+
+@pytest.mark.parametrize("prec,d,n,l,k", [("fp32", 32, 50_000, 256, 10), ("fp16", 128, 20_011, 300, 6)])
+def test_chunking_target_keeps_the_bits(torch_gpu, monkeypatch, prec, d, n, l, k):
+    """EXEMCL_WG_TARGET only changes how set groups are grouped into chunks
+    (one workgroup walks a chunk over its rows): every set's partial sums
+    come out the same, from one chunk of all groups to one chunk per group."""
+    torch = torch_gpu
+    p = synth.random_problem(n, d, l, k, seed=900 + d, clusters=5)
+    Vg, _ = to_gpu(torch, p.X, prec)
+    base = gpu_eval(torch, Vg, p.sets)
+    for target in ("1", "300", "1000000"):
+        monkeypatch.setenv("EXEMCL_WG_TARGET", target)
+        say(f"chunking target {target}: prec={prec} n={n} d={d} l={l} k={k}")
+        assert np.array_equal(gpu_eval(torch, Vg, p.sets), base)
