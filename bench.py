@@ -7,8 +7,9 @@ second pass) for eval workloads, exemplar_gain (cache + scoring) for greedy
 workloads.  Inputs are synthetic, seeded, and resident in HBM before timing
 starts.  Prints one JSON line on stdout; progress goes to stderr.
 
-Default workload: 50 000 points of a 10-Gaussian mixture in d = 32 (fp32),
-256 sets of 10 exemplars.
+Default workload (the largest single-GPU configuration): 1 000 000 points of
+a 100-Gaussian mixture in d = 256, stored as fp16 (fp32 accumulate), 2 048
+sets of 32 exemplars.
 """
 from __future__ import annotations
 
@@ -483,7 +484,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=None,
                     help=f"untimed warm-up steps (default: {WARMUP_SECONDS} s of back-to-back steps, "
                          f"at least {MIN_WARMUP})")
-    ap.add_argument("--workload", default="mix50k", choices=sorted(synth.WORKLOADS))
+    ap.add_argument("--workload", default="large1m", choices=sorted(synth.WORKLOADS))
     ap.add_argument("--cpu-budget", type=float, default=10.0, help="seconds of oracle time for the CPU baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe", action="store_true", help="run a plain 1 GiB device copy (counter calibration)")

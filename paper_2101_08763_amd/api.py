@@ -187,10 +187,14 @@ def exemplar_gain(V, S, cands, out=None, stream=None):
         raise TypeError("exemplar_gain takes float32 V")
     if S.dtype != torch.int32 or cands.dtype != torch.int32:
         raise TypeError("S and cands must be int32")
+    if V.dim() != 2:
+        raise ValueError("V must be n x d")
     n, d = V.shape
     l = cands.numel()
     if out is None:
         out = torch.empty(l, dtype=torch.float32, device=V.device)
+    elif out.dtype != torch.float32 or out.numel() != l:
+        raise ValueError("out must be float32 with one element per candidate")
     with _device_scope(_check_device(V, S if S.numel() else None, cands, out)):
         rc = load().exemplar_gain(_ptr(V), n, d, _ptr(S), S.numel(), _ptr(cands), l, _ptr(out),
                                   _stream(stream))

@@ -6,6 +6,13 @@ Tolerance (|gpu - oracle| <= rtol*|oracle| + atol):
                      the rounded values the GPU saw.
 The absolute floor is needed where f is near 0 (k = 0, e0-like exemplars).
 Index handling (which set is NaN, which result lands in which slot) is exact.
+
+On top of that gate, the full-size workloads and the d sweep assert the
+arithmetic bound of the kernels (``exact``): relative error at most 1e-5
+against the oracle run on the very values the GPU read, in every precision.
+fp16/bf16 products are exact in fp32, so reduced-precision storage adds no
+error beyond fp32 accumulation; a dropped or misplaced block of coordinates
+or member would break this bound even where it hides under 2e-2.
 """
 import os
 import sys
@@ -20,6 +27,7 @@ pytestmark = pytest.mark.gpu
 
 RTOL = {"fp32": 1e-5, "fp16": 2e-2, "bf16": 2e-2}
 ATOL = {"fp32": 1e-7, "fp16": 1e-4, "bf16": 1e-4}
+EXACT_RTOL = 1e-5   # fp32 accumulation bound, every storage type
 
 
 def say(*a):
@@ -72,6 +80,22 @@ def check(got, want, le0, prec, what):
     assert np.all(err <= bound), f"{what}: max excess {(err - bound).max():.3e}"
 
 
+def exact(got, want, what):
+    """Relative error against the oracle on the same (rounded) inputs at most
+    EXACT_RTOL for every value; exact zeros must come out as zeros."""
+    got = np.asarray(got, np.float64)
+    want = np.asarray(want, np.float64)
+    ok = ~np.isnan(want)
+    assert np.array_equal(np.isnan(got), ~ok), f"{what}: NaN pattern differs"
+    nz = ok & (want != 0.0)
+    assert np.all(got[ok & (want == 0.0)] == 0.0), f"{what}: nonzero result where f = 0"
+    rel = np.abs(got[nz] - want[nz]) / np.abs(want[nz])
+    worst = float(rel.max()) if rel.size else 0.0
+    say(f"  {what}: {int(nz.sum())} values, max rel err {worst:.3e} (exact bound {EXACT_RTOL:.0e})")
+    assert worst <= EXACT_RTOL, f"{what}: max rel err {worst:.3e} above {EXACT_RTOL:.0e}"
+    return worst
+
+
 # ---------------------------------------------------------------------------
 # The tiny 1 000-point workload, on both paths.
 # ---------------------------------------------------------------------------
@@ -113,17 +137,19 @@ def test_ragged_valu(torch_gpu, orc, monkeypatch, prec, d):
 
 
 @pytest.mark.parametrize("prec", ["fp16", "bf16"])
-@pytest.mark.parametrize("d", [2, 16, 64])
+@pytest.mark.parametrize("d", [2, 16, 64, 100, 128, 200, 256, 300, 512])
 def test_half_inputs_are_exact_in_fp32(torch_gpu, orc, prec, d):
     """fp16/bf16 products are exact in fp32, so against the oracle on the
     rounded inputs the error is fp32 accumulation only.  At d <= 16 the bias
     seeds the accumulators through a bf16 MFMA of its three-part split, which
-    must be exact too."""
+    must be exact too; d = 100 and 200 end in a half k-block of 16
+    coordinates (16x16x16 instruction), 300 in a zero-padded one."""
     p = synth.random_problem(3000, d, 40, 11, seed=77 + d, clusters=5)
     Vg, X64 = to_gpu(torch_gpu, p.X, prec)
     got = gpu_eval(torch_gpu, Vg, p.sets)
     want = orc.eval(X64, p.sets, 8)
-    assert np.max(np.abs(got - want) / np.abs(want)) < 1e-5
+    check(got, want, orc.loss_e0(X64), prec, f"d={d}")
+    exact(got, want, f"{prec} d={d} vs rounded-input oracle")
 
 
 # ---------------------------------------------------------------------------
@@ -131,6 +157,7 @@ def test_half_inputs_are_exact_in_fp32(torch_gpu, orc, prec, d):
 # strided sample of sets.
 # ---------------------------------------------------------------------------
 def strided(l, m):
+    """m strided positions of [0, l), the first and the last included."""
     if l <= m:
         return np.arange(l)
     return np.unique((np.arange(m) * (l - 1)) // (m - 1))
@@ -141,7 +168,9 @@ def test_mix50k_all_sets(torch_gpu, orc):
     say("mix50k: 50 000 x 32 fp32, 256 sets of 10")
     Vg, X64 = to_gpu(torch_gpu, p.X, "fp32")
     got = gpu_eval(torch_gpu, Vg, p.sets)
-    check(got, orc.eval(X64, p.sets, 0), orc.loss_e0(X64), "fp32", "mix50k")
+    want = orc.eval(X64, p.sets, 0)
+    check(got, want, orc.loss_e0(X64), "fp32", "mix50k")
+    exact(got, want, "mix50k")
 
 
 @pytest.mark.parametrize("d", [2, 16, 128, 512])
@@ -151,8 +180,10 @@ def test_sweep_sampled(torch_gpu, orc, d, prec):
     say(f"sweep d={d} {prec}: 100 000 points, 1024 sets of 16")
     Vg, X64 = to_gpu(torch_gpu, p.X, prec)
     got = gpu_eval(torch_gpu, Vg, p.sets)
-    idx = strided(len(p.sets), 16 if d >= 128 else 64)
-    check(got[idx], orc.eval(X64, p.sets[idx], 0), orc.loss_e0(X64), prec, f"sweep d={d}")
+    idx = strided(len(p.sets), 64)
+    want = orc.eval(X64, p.sets[idx], 0)
+    check(got[idx], want, orc.loss_e0(X64), prec, f"sweep d={d}")
+    exact(got[idx], want, f"sweep d={d} {prec}")
     assert np.all(np.isfinite(got)) and np.all(got >= 0)
 
 
@@ -182,19 +213,31 @@ def test_greedy200k_sampled(torch_gpu, orc):
     got = api.exemplar_gain(Vg, S, C)
     torch_gpu.cuda.synchronize()
     got = got.cpu().numpy().astype(np.float64)
-    idx = strided(len(p.cands), 32)
-    check(got[idx], orc.gain(X64, p.S, p.cands[idx], 0), orc.loss_e0(X64), "fp32", "greedy200k")
+    idx = strided(len(p.cands), 64)
+    want = orc.gain(X64, p.S, p.cands[idx], 0)
+    check(got[idx], want, orc.loss_e0(X64), "fp32", "greedy200k")
+    exact(got[idx], want, "greedy200k")
 
 
 @pytest.mark.slow
-def test_large1m_sampled(torch_gpu, orc):
-    p = synth.make("large1m")
+def test_large1m_sampled(torch_gpu, large1m_ref):
+    """The benchmark's default workload in its benchmark launch: all 2 048
+    sets on the GPU, 64 strided ones (first and last included) against the
+    oracle on the fp16 values.  Also reported, not gated: how far the fp16
+    results are from f on the fp32 data before rounding (the effect of half
+    precision storage, which the paper leaves open)."""
+    r = large1m_ref
+    p, idx = r["p"], r["idx"]
     say("large1m: 1 000 000 x 256 fp16, 2048 sets of 32")
-    Vg, X64 = to_gpu(torch_gpu, p.X, "fp16")
+    Vg, _ = to_gpu(torch_gpu, p.X, "fp16")
     got = gpu_eval(torch_gpu, Vg, p.sets)
-    idx = strided(len(p.sets), 4)
-    check(got[idx], orc.eval(X64, p.sets[idx], 0), orc.loss_e0(X64), "fp16", "large1m")
     assert np.all(np.isfinite(got)) and np.all(got >= 0)
+    check(got[idx], r["want"], r["le0"], "fp16", "large1m")
+    exact(got[idx], r["want"], "large1m vs rounded-input oracle")
+    w32 = r["fp32_values"]()
+    dev = np.abs(got[idx] - w32) / np.abs(w32)
+    say(f"  large1m fp16 storage vs f on the fp32 data (not gated): max rel {dev.max():.3e}, "
+        f"median {np.median(dev):.3e}, mean signed {np.mean((got[idx] - w32) / w32):+.3e}")
 
 
 # ---------------------------------------------------------------------------
