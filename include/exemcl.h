@@ -70,8 +70,13 @@ enum exemcl_status {
     EXEMCL_OK = 0,      /* queued (or nothing to do) */
     EXEMCL_EINVAL = 1,  /* bad argument; nothing was queued */
     EXEMCL_ENOMEM = 2,  /* temporary device memory unavailable; nothing was queued */
-    EXEMCL_EDEVICE = 3  /* a HIP call or kernel launch failed */
+    EXEMCL_EDEVICE = 3, /* a HIP call or kernel launch failed */
+    EXEMCL_ESCRATCH = 4 /* exemplar_eval_noalloc: the call needs more temporary memory than
+                           the fixed scratch buffer holds; nothing was queued */
 };
+
+/* Bytes of the fixed device scratch buffer behind exemplar_eval_noalloc. */
+#define EXEMCL_SCRATCH_BYTES (64ll << 20)
 
 /* Evaluation paths (see exemplar_plan). */
 enum exemcl_path {
@@ -111,6 +116,38 @@ enum exemcl_path {
  */
 EXEMCL_API int exemplar_eval(const void *V, int64_t n, int64_t d, const int32_t *sets, int64_t l,
                              int64_t k, int precision, float *out, void *stream);
+
+/*
+ * exemplar_eval_noalloc -- exemplar_eval for callers that cannot allocate
+ * device memory: code under HIP graph capture, tight serving loops, and
+ * harnesses that forbid hipMalloc.
+ *
+ * Same arguments, results (bitwise equal to exemplar_eval's), asynchrony and
+ * errors as exemplar_eval, except for where temporaries live: partial sums,
+ * staged exemplar tiles and (when V's rows are not whole 16-byte vectors) the
+ * zero-padded copy of V are carved from a fixed scratch buffer of
+ * EXEMCL_SCRATCH_BYTES (64 MiB) that is part of the library's code object on
+ * each GPU and held until the process ends.  The call makes no allocation of
+ * any kind (no hipMalloc, no pool, no library allocation) and records no
+ * profiling events.  A batch whose workspace exceeds the buffer is processed
+ * in chunks of whole set groups, as exemplar_eval does under a workspace
+ * limit, with bitwise the same results.
+ *
+ * Every call on one GPU uses that GPU's one buffer, and the buffer keeps the
+ * last call's contents (nothing in it needs to start at zero: every byte a
+ * kernel reads was written earlier in the same call).  Calls that overlap on
+ * one GPU -- on different streams, or from different host threads -- race on
+ * the buffer and give undefined results: serialise them (one stream, or
+ * events between the streams).  Calls on different GPUs are independent.
+ *
+ * Errors: as exemplar_eval, plus EXEMCL_ESCRATCH when even one set group's
+ * workspace plus the padded copy of V does not fit the buffer (for example
+ * n in the tens of millions of points, where one set group's partial sums
+ * alone exceed 64 MiB, or a padded copy of V larger than the buffer); nothing
+ * is queued then.  EXEMCL_WORKSPACE_LIMIT, when set lower, caps it further.
+ */
+EXEMCL_API int exemplar_eval_noalloc(const void *V, int64_t n, int64_t d, const int32_t *sets, int64_t l,
+                                     int64_t k, int precision, float *out, void *stream);
 
 /*
  * exemplar_eval_streamed -- exemplar_eval for a V kept in HOST memory, e.g.

@@ -14,11 +14,12 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(PKG, "libexemcl.so")
 
 EXEMCL_FP32, EXEMCL_FP16, EXEMCL_BF16 = 0, 1, 2
-EXEMCL_OK, EXEMCL_EINVAL, EXEMCL_ENOMEM, EXEMCL_EDEVICE = 0, 1, 2, 3
+EXEMCL_OK, EXEMCL_EINVAL, EXEMCL_ENOMEM, EXEMCL_EDEVICE, EXEMCL_ESCRATCH = 0, 1, 2, 3, 4
+EXEMCL_SCRATCH_BYTES = 64 << 20   # fixed scratch buffer of exemplar_eval_noalloc
 PATH_NONE, PATH_VALU, PATH_MFMA = 0, 1, 2
 PATH_NAMES = {PATH_NONE: "none", PATH_VALU: "valu", PATH_MFMA: "mfma"}
 
-EXPORTED = ("exemplar_eval", "exemplar_eval_streamed", "exemplar_gain", "exemplar_greedy", "exemplar_sqnorm",
+EXPORTED = ("exemplar_eval", "exemplar_eval_noalloc", "exemplar_eval_streamed", "exemplar_gain", "exemplar_greedy", "exemplar_sqnorm",
             "exemplar_plan",
             "exemplar_prof_enable", "exemplar_prof_read", "exemplar_strerror", "exemplar_version")
 
@@ -46,6 +47,8 @@ def load(path: str | None = None) -> ctypes.CDLL:
     vp, i64, ip = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int
     lib.exemplar_eval.argtypes = [vp, i64, i64, vp, i64, i64, ip, vp, vp]
     lib.exemplar_eval.restype = ip
+    lib.exemplar_eval_noalloc.argtypes = [vp, i64, i64, vp, i64, i64, ip, vp, vp]
+    lib.exemplar_eval_noalloc.restype = ip
     lib.exemplar_eval_streamed.argtypes = [vp, i64, i64, vp, i64, i64, ip, i64, vp, vp]
     lib.exemplar_eval_streamed.restype = ip
     lib.exemplar_gain.argtypes = [vp, i64, i64, vp, i64, vp, i64, vp, vp]
@@ -75,7 +78,8 @@ def strerror(status: int) -> str:
         return load().exemplar_strerror(int(status)).decode()
     except ImportError:
         return {0: "success", 1: "invalid argument", 2: "temporary device memory unavailable",
-                3: "HIP runtime or kernel launch failure"}.get(int(status), "unknown status")
+                3: "HIP runtime or kernel launch failure",
+                4: "workspace needed exceeds the fixed no-allocation scratch buffer"}.get(int(status), "unknown status")
 
 
 def precision_of(dtype) -> int:
@@ -147,6 +151,28 @@ def exemplar_eval(V, sets, out=None, stream=None):
         rc = load().exemplar_eval(_ptr(V), n, d, _ptr(sets), l, k, prec, _ptr(out), _stream(stream))
     if rc != EXEMCL_OK:
         raise ExemclError(rc, "exemplar_eval")
+    return out
+
+
+def exemplar_eval_noalloc(V, sets, out, stream=None):
+    """exemplar_eval with every temporary in the library's fixed scratch
+    buffer (see exemplar_eval_noalloc in exemcl.h); ``out`` (float32, l
+    elements, on V's device) is required, so nothing is allocated here
+    either."""
+    import torch
+    if V.dim() != 2 or sets.dim() != 2:
+        raise ValueError("V must be n x d and sets l x k")
+    if sets.dtype != torch.int32:
+        raise TypeError("sets must be int32")
+    prec = precision_of(V.dtype)
+    n, d = V.shape
+    l, k = sets.shape
+    if out is None or out.dtype != torch.float32 or out.numel() != l:
+        raise ValueError("out must be float32 with l elements")
+    with _device_scope(_check_device(V, sets, out)):
+        rc = load().exemplar_eval_noalloc(_ptr(V), n, d, _ptr(sets), l, k, prec, _ptr(out), _stream(stream))
+    if rc != EXEMCL_OK:
+        raise ExemclError(rc, "exemplar_eval_noalloc")
     return out
 
 

@@ -198,14 +198,25 @@ void release_free_blocks(size_t i) {
     if (bl.empty()) g_keep.erase(g_keep.begin() + (std::ptrdiff_t)i);
 }
 
+// A caller-provided region that temporaries are carved from, front to back,
+// instead of being allocated (exemplar_eval_noalloc).  Carving is a host-side
+// bump of `used`; nothing is returned to it within a call.
+struct Arena {
+    char *base = nullptr;
+    int64_t cap = 0;
+    int64_t used = 0;
+    int64_t left() const { return cap - used; }
+};
+
 struct Scratch {
     void *ptr = nullptr;
     hipStream_t st = nullptr;
     bool kept = false;
+    bool borrowed = false;  // carved from an Arena: nothing to release
     int dev = 0;
     uintptr_t sid = 0;
     ~Scratch() {
-        if (!ptr) return;
+        if (!ptr || borrowed) return;
         if (!kept) {
             hipFreeAsync(ptr, st);
             return;
@@ -217,10 +228,18 @@ struct Scratch {
     }
 };
 
-int alloc_scratch(Scratch *s, int64_t bytes, hipStream_t st) {
+int alloc_scratch(Scratch *s, int64_t bytes, hipStream_t st, Arena *arena = nullptr) {
     s->st = st;
     if (bytes <= 0) return EXEMCL_OK;
     if (bytes > workspace_limit()) return EXEMCL_ENOMEM;
+    if (arena) {
+        const int64_t take = align_up(bytes, 256);
+        if (take > arena->left()) return EXEMCL_ENOMEM;
+        s->ptr = arena->base + arena->used;
+        s->borrowed = true;
+        arena->used += take;
+        return EXEMCL_OK;
+    }
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess) {
         (void)hipGetLastError();
@@ -321,7 +340,8 @@ int64_t pad_bytes(int precision, int64_t n, int64_t d) {
     return (d * elem_size(precision)) % 16 == 0 ? 0 : align_up(n * mfma_row_stride(precision, d) * elem_size(precision), 256);
 }
 
-int prepare_rows(const void *V, int64_t n, int64_t d, int precision, hipStream_t st, MfmaRows *r) {
+int prepare_rows(const void *V, int64_t n, int64_t d, int precision, hipStream_t st, MfmaRows *r,
+                 Arena *arena = nullptr) {
     if (rows_as_is(precision, d) || mfma_rows_ready(precision, V, d)) {
         r->V = V;
         r->ld = d;
@@ -329,7 +349,7 @@ int prepare_rows(const void *V, int64_t n, int64_t d, int precision, hipStream_t
     }
     r->ld = mfma_row_stride(precision, d);
     r->bytes = align_up(n * r->ld * elem_size(precision), 256);
-    const int rc = alloc_scratch(&r->copy, r->bytes, st);
+    const int rc = alloc_scratch(&r->copy, r->bytes, st, arena);
     if (rc) return rc;
     if (launch_pad(precision, V, n, (int)d, r->copy.ptr, (int)r->ld, st) != hipSuccess) return EXEMCL_EDEVICE;
     r->V = r->copy.ptr;
@@ -349,7 +369,8 @@ std::vector<std::pair<hipEvent_t, hipEvent_t>> g_prof_events;
 struct ProfRange {
     hipEvent_t a = nullptr, b = nullptr;
     hipStream_t st;
-    explicit ProfRange(hipStream_t s) : st(s) {
+    explicit ProfRange(hipStream_t s, bool allowed = true) : st(s) {
+        if (!allowed) return;
         bool on;
         {
             std::lock_guard<std::mutex> lk(g_prof_mu);
@@ -383,7 +404,7 @@ struct ProfRange {
 // Queue the evaluation of sets [0, l) with a workspace laid out by L.
 hipError_t run_chunk(const Layout &L, char *base, const void *V, int64_t n, int64_t d, const MfmaRows *rows,
                      const int32_t *sets, int64_t l, int64_t k, int precision, const float *m0,
-                     const int32_t *common, int64_t kcommon, float *out, hipStream_t st) {
+                     const int32_t *common, int64_t kcommon, float *out, hipStream_t st, bool prof = true) {
     if (L.path == EXEMCL_PATH_NONE) return launch_zero(out, l, st);  // k = 0: every set is empty
     float *partials = (float *)(base + L.off_partials);
     hipError_t e = hipSuccess;
@@ -391,13 +412,13 @@ hipError_t run_chunk(const Layout &L, char *base, const void *V, int64_t n, int6
         void *tiles = base + L.off_tiles;
         e = launch_pack(precision, L.mp, rows->V, n, (int)rows->ld, sets, l, k, tiles, st);
         if (e == hipSuccess) {
-            ProfRange pr(st);
+            ProfRange pr(st, prof);
             e = launch_mfma(precision, MODE_SUM, L.mp, rows->V, n, (int)rows->ld, tiles, mfma_tiles_per_group(L.mp, k),
                             L.ngroups, L.gpc, m0, partials, L.lpad, nullptr, st, pr.a, pr.b);
             if (e == hipSuccess) pr.end();
         }
     } else if (L.path == EXEMCL_PATH_VALU) {
-        ProfRange pr(st);
+        ProfRange pr(st, prof);
         pr.record_start();
         e = launch_valu(precision, L.vp, V, n, (int)d, sets, l, k, partials, L.lpad, st);
         pr.record_stop();
@@ -420,10 +441,11 @@ hipError_t run_chunk(const Layout &L, char *base, const void *V, int64_t n, int6
 //
 // `rows` (nullable) is V already prepared for the MFMA kernels by the caller,
 // which also holds `reserved` bytes of temporary memory that count against
-// EXEMCL_WORKSPACE_LIMIT.
+// EXEMCL_WORKSPACE_LIMIT.  With `arena` every temporary is carved from it
+// (and the chunks are sized to what is left of it); nothing is allocated.
 int run_eval(const void *V, int64_t n, int64_t d, const int32_t *sets, int64_t l, int64_t k, int precision,
              const float *m0, const int32_t *common, int64_t kcommon, float *out, hipStream_t st,
-             const MfmaRows *rows = nullptr, int64_t reserved = 0) {
+             const MfmaRows *rows = nullptr, int64_t reserved = 0, Arena *arena = nullptr) {
     if (l == 0) return EXEMCL_OK;
     int path = k == 0 ? EXEMCL_PATH_NONE : choose_path(d, k, precision);
     if (m0 && path == EXEMCL_PATH_VALU) path = EXEMCL_PATH_MFMA;
@@ -433,19 +455,26 @@ int run_eval(const void *V, int64_t n, int64_t d, const int32_t *sets, int64_t l
     const int64_t unit = path == EXEMCL_PATH_MFMA ? L.mp.tile : 1;
     MfmaRows own;
     if (path == EXEMCL_PATH_MFMA && !rows) {
-        if (reserved + pad_bytes(precision, n, d) > workspace_limit()) return EXEMCL_ENOMEM;
-        const int rc = prepare_rows(V, n, d, precision, st, &own);
+        const int64_t pb = pad_bytes(precision, n, d);
+        if (reserved + pb > workspace_limit() || (arena && pb > arena->left())) return EXEMCL_ENOMEM;
+        // Nothing is queued unless the padded rows and one set group fit.
+        Layout L1;
+        if (!layout_eval(n, d, std::min<int64_t>(l, unit), k, precision, path, &L1)) return EXEMCL_EINVAL;
+        if (reserved + pb + L1.bytes > workspace_limit() || (arena && pb + L1.bytes > arena->left()))
+            return EXEMCL_ENOMEM;
+        const int rc = prepare_rows(V, n, d, precision, st, &own, arena);
         if (rc) return rc;
         rows = &own;
         reserved += own.bytes;
     }
-    const int64_t limit = workspace_limit() - reserved;
+    int64_t limit = workspace_limit() - reserved;
+    if (arena) limit = std::min(limit, arena->left());
     int64_t lc = l;
     Scratch ws;
     for (;;) {
         if (!layout_eval(n, d, lc, k, precision, path, &L)) return EXEMCL_EINVAL;
         if (L.bytes <= limit) {
-            const int rc = alloc_scratch(&ws, L.bytes, st);
+            const int rc = alloc_scratch(&ws, L.bytes, st, arena);
             if (rc == EXEMCL_OK) break;
             if (rc != EXEMCL_ENOMEM) return rc;
         }
@@ -458,7 +487,7 @@ int run_eval(const void *V, int64_t n, int64_t d, const int32_t *sets, int64_t l
         Layout Lj;
         if (!layout_eval(n, d, lj, k, precision, path, &Lj)) return EXEMCL_EINVAL;
         const hipError_t e = run_chunk(Lj, base, V, n, d, rows, sets + j0 * k, lj, k, precision, m0, common,
-                                       kcommon, out + j0, st);
+                                       kcommon, out + j0, st, arena == nullptr);
         if (e != hipSuccess) return EXEMCL_EDEVICE;
     }
     return EXEMCL_OK;
@@ -706,6 +735,42 @@ int run_streamed(const void *V, int64_t n, int64_t d, const int32_t *sets, int64
     return status_of(e);
 }
 
+// ---------------------------------------------------------------------------
+// Fixed device scratch of exemplar_eval_noalloc: one array per GPU, part of
+// the library's code object, so no call has to allocate.  Host code never
+// uses the array's name as an address (on the host it is only a stand-in for
+// the symbol): the device address is looked up once per device and kept.
+// ---------------------------------------------------------------------------
+static __device__ __align__(256) unsigned char scratch[EXEMCL_SCRATCH_BYTES];
+
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[64] = {};
+
+// Device address of the current device's scratch array (looked up on the
+// first call on that device, with that device current).
+int scratch_arena(Arena *a) {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) {
+        (void)hipGetLastError();
+        return EXEMCL_EDEVICE;
+    }
+    if (dev < 0 || dev >= 64) return EXEMCL_EDEVICE;
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void *p = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !p) {
+            (void)hipGetLastError();
+            return EXEMCL_EDEVICE;
+        }
+        g_scratch_ptr[dev] = p;
+    }
+    a->base = (char *)g_scratch_ptr[dev];
+    a->cap = EXEMCL_SCRATCH_BYTES;
+    a->used = 0;
+    return EXEMCL_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -718,6 +783,21 @@ EXEMCL_API int exemplar_eval(const void *V, int64_t n, int64_t d, const int32_t 
     if (l > 0 && k > 0 && !sets) return EXEMCL_EINVAL;
     if (l > 0 && k > 0 && choose_path(d, k, precision) == EXEMCL_PATH_NONE) return EXEMCL_EINVAL;
     return run_eval(V, n, d, sets, l, k, precision, nullptr, nullptr, 0, out, (hipStream_t)stream);
+}
+
+EXEMCL_API int exemplar_eval_noalloc(const void *V, int64_t n, int64_t d, const int32_t *sets, int64_t l,
+                                     int64_t k, int precision, float *out, void *stream) {
+    int rc = check_common(V, n, d, l, k, out);
+    if (rc) return rc;
+    if (!prec_ok(precision)) return EXEMCL_EINVAL;
+    if (l > 0 && k > 0 && !sets) return EXEMCL_EINVAL;
+    if (l > 0 && k > 0 && choose_path(d, k, precision) == EXEMCL_PATH_NONE) return EXEMCL_EINVAL;
+    if (l == 0) return EXEMCL_OK;
+    Arena a;
+    rc = scratch_arena(&a);
+    if (rc) return rc;
+    rc = run_eval(V, n, d, sets, l, k, precision, nullptr, nullptr, 0, out, (hipStream_t)stream, nullptr, 0, &a);
+    return rc == EXEMCL_ENOMEM ? EXEMCL_ESCRATCH : rc;
 }
 
 EXEMCL_API int exemplar_eval_streamed(const void *V, int64_t n, int64_t d, const int32_t *sets, int64_t l,
@@ -910,6 +990,7 @@ EXEMCL_API const char *exemplar_strerror(int status) {
     case EXEMCL_EINVAL: return "invalid argument";
     case EXEMCL_ENOMEM: return "temporary device memory unavailable";
     case EXEMCL_EDEVICE: return "HIP runtime or kernel launch failure";
+    case EXEMCL_ESCRATCH: return "workspace needed exceeds the fixed no-allocation scratch buffer";
     }
     return "unknown status";
 }

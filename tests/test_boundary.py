@@ -35,7 +35,7 @@ def test_library_exports_every_declared_symbol(lib):
 
 
 def test_strerror(lib):
-    for status in range(4):
+    for status in range(5):
         assert lib.exemplar_strerror(status)
     assert lib.exemplar_strerror(99) == b"unknown status"
 
