@@ -316,6 +316,26 @@ __global__ __launch_bounds__(64) void pack_tiles_kernel(const T *__restrict__ V,
 #ifndef EXEMCL_RING_BIG
 #define EXEMCL_RING_BIG 3
 #endif
+#ifndef EXEMCL_TPS_FILL_MAX
+#define EXEMCL_TPS_FILL_MAX 8
+#endif
+// fp16/bf16 two-member tiles of at least EXEMCL_WIDE16_MIN_NKB k-blocks run
+// as one 8-wavefront workgroup per CU (their registers allow two wavefronts
+// per SIMD either way): the CU's eight wavefronts share each staged tile and
+// advance together, and the persistent launch gives every CU equal work.
+#ifndef EXEMCL_WIDE16_MIN_NKB
+#define EXEMCL_WIDE16_MIN_NKB 6
+#endif
+// Shorter two-member tiles (EXEMCL_W12_MIN_NKB .. EXEMCL_WIDE16_MIN_NKB - 1
+// k-blocks) fit three wavefronts per SIMD: one 12-wavefront workgroup per CU.
+#ifndef EXEMCL_W12_MIN_NKB
+#define EXEMCL_W12_MIN_NKB 2
+#endif
+// ... and tiles of at most EXEMCL_W16_MAX_NKB k-blocks four per SIMD: one
+// 16-wavefront workgroup per CU.
+#ifndef EXEMCL_W16_MAX_NKB
+#define EXEMCL_W16_MAX_NKB 1
+#endif
 
 constexpr int kLdsBytes = 160 * 1024;
 
@@ -332,23 +352,27 @@ constexpr int lds_budget() {
     return WAVES <= 4 ? kLdsBytes / 2 : kLdsBytes;
 }
 
-// Stage geometry for tiles of TB bytes and NFRAG B fragments.
-template <int TB, int NFRAG, int WAVES>
+// Stage geometry for tiles of TB bytes and NFRAG B fragments.  FILL (8
+// wavefronts, two-member tiles: one workgroup per CU in lockstep) takes as
+// many tiles per stage as two stages fit in the LDS, since the cost of a
+// stage is its barrier, which every wavefront of the CU waits at.
+template <int TB, int NFRAG, int WAVES, bool FILL = false>
 constexpr int tiles_per_stage() {
-    int tps = NFRAG <= EXEMCL_BIG_NKB ? (EXEMCL_STAGE_MIN / TB > 1 ? EXEMCL_STAGE_MIN / TB : 1) : EXEMCL_TPS_BIG;
+    int tps = FILL ? EXEMCL_TPS_FILL_MAX
+                   : NFRAG <= EXEMCL_BIG_NKB ? (EXEMCL_STAGE_MIN / TB > 1 ? EXEMCL_STAGE_MIN / TB : 1) : EXEMCL_TPS_BIG;
     while (tps > 1 && 2 * round_stage<NFRAG, WAVES>(tps * TB) > lds_budget<WAVES>()) --tps;
     return tps;
 }
 
-template <int TB, int NFRAG, int WAVES>
+template <int TB, int NFRAG, int WAVES, bool FILL = false>
 constexpr int stage_bytes() {
-    return round_stage<NFRAG, WAVES>(tiles_per_stage<TB, NFRAG, WAVES>() * TB);
+    return round_stage<NFRAG, WAVES>(tiles_per_stage<TB, NFRAG, WAVES, FILL>() * TB);
 }
 
-template <int TB, int NFRAG, int WAVES>
+template <int TB, int NFRAG, int WAVES, bool FILL = false>
 constexpr int ring_depth() {
-    constexpr int want = NFRAG <= EXEMCL_BIG_NKB ? EXEMCL_RING_SMALL : EXEMCL_RING_BIG;
-    constexpr int sb = stage_bytes<TB, NFRAG, WAVES>();
+    constexpr int want = FILL ? 2 : NFRAG <= EXEMCL_BIG_NKB ? EXEMCL_RING_SMALL : EXEMCL_RING_BIG;
+    constexpr int sb = stage_bytes<TB, NFRAG, WAVES, FILL>();
     constexpr int fit = (sb * 2 <= lds_budget<WAVES>() ? lds_budget<WAVES>() : kLdsBytes) / sb;
     return want < fit ? want : fit;
 }
@@ -431,10 +455,11 @@ __global__ __launch_bounds__(WAVES * 64, PERSIST ? 2 : 1) void eval_mfma_kernel(
     constexpr int NBIAS = SPLAT ? 2 : NB;  // bias registers per tile (SPLAT: the 8 header bytes)
     constexpr int HDR = hdr_bytes(TM, NB, SPLAT);
     constexpr int TB = tile_bytes_of(HDR, NFF, HALF ? NB : 0);
-    constexpr int SB = stage_bytes<TB, NF, WAVES>();
-    constexpr int TPS = tiles_per_stage<TB, NF, WAVES>();
+    constexpr bool FILL = WAVES >= 8 && NB == 2;
+    constexpr int SB = stage_bytes<TB, NF, WAVES, FILL>();
+    constexpr int TPS = tiles_per_stage<TB, NF, WAVES, FILL>();
     constexpr int CNT = SB / (NT * 16);
-    constexpr int NBUF = ring_depth<TB, NF, WAVES>();
+    constexpr int NBUF = ring_depth<TB, NF, WAVES, FILL>();
     static_assert(!HALF || (M::HAS_HALF && NKB >= 2), "half k-block needs the 16x16x16 instruction and a whole block");
     // Reads across tiles pay off for long tiles; short ones keep the registers
     // for a third wavefront per SIMD instead.
@@ -705,11 +730,26 @@ __global__ __launch_bounds__(WAVES * 64, PERSIST ? 2 : 1) void eval_mfma_kernel(
     int g = (int)g0;
     int p = 0;
     const int nst = (int)nstages;
+    // Close set group g after its last tile has been folded: sum this lane's
+    // rows for its column, then the K-groups holding the other rows of the
+    // same column; store, and start group g + 1.
+    auto group_end = [&]() {
+        if constexpr (MODE == MODE_SUM) {
+            float sum = lane_sum();
+#pragma unroll
+            for (int off = TM; off < 64; off <<= 1) sum += __shfl_xor(sum, off);
+            if (grp == 0) wpart[(int64_t)g * TM + lr] = sum;
+#pragma unroll
+            for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+                for (int i = 0; i < M::ACC; ++i) m[rt][i] = m_init(rt, i);
+        }
+        ++g;
+    };
     for (int s = 0; s < nst; ++s) {
         if (s + NBUF - 2 < nst) wait_vmcnt<CNT * (NBUF - 2)>();
         else wait_vmcnt<0>();
         __syncthreads();
-        if (s + NBUF - 1 < nst) issue(s + NBUF - 1);
 
         const unsigned char *buf = smem + (s % NBUF) * SB;
         const int tn = (int)min((int64_t)TPS, ntiles - (int64_t)s * TPS);
@@ -718,22 +758,10 @@ __global__ __launch_bounds__(WAVES * 64, PERSIST ? 2 : 1) void eval_mfma_kernel(
         float bias[NBIAS];
 #pragma unroll
         for (int h = 0; h < NBIAS; ++h) bias[h] = 0.0f;
+        // The stage's first fragments are read before the next stage's copy
+        // is queued, so their LDS latency overlaps the copy's issue.
         if constexpr (SCHED) head(buf, bq, bias);
-        // Close set group g after its last tile: sum this lane's rows for
-        // its column, then the K-groups holding the other rows of the same
-        // column.
-        auto group_end = [&]() {
-            if constexpr (MODE == MODE_SUM) {
-                float sum = lane_sum();
-#pragma unroll
-                for (int off = TM; off < 64; off <<= 1) sum += __shfl_xor(sum, off);
-                if (grp == 0) wpart[(int64_t)g * TM + lr] = sum;
-#pragma unroll
-                for (int rt = 0; rt < RT; ++rt)
-#pragma unroll
-                    for (int i = 0; i < M::ACC; ++i) m[rt][i] = m_init(rt, i);
-            }
-        };
+        if (s + NBUF - 1 < nst) issue(s + NBUF - 1);
         if constexpr (PAIR && NKB == 1) {
             // Tiles of one k-block hold a few MFMAs each: the operands of the
             // next pair are read from LDS while this pair is folded (a
@@ -758,7 +786,6 @@ __global__ __launch_bounds__(WAVES * 64, PERSIST ? 2 : 1) void eval_mfma_kernel(
                     if (p == ktile) {
                         group_end();
                         p = 0;
-                        ++g;
                     }
                 }
                 if (tt < tn) {
@@ -769,7 +796,6 @@ __global__ __launch_bounds__(WAVES * 64, PERSIST ? 2 : 1) void eval_mfma_kernel(
                     if (++p == ktile) {
                         group_end();
                         p = 0;
-                        ++g;
                     }
                     head(tile_at(tt), bqa, ba);
                     head(tile_at(tt + 1), bqb, bbb);
@@ -793,7 +819,6 @@ __global__ __launch_bounds__(WAVES * 64, PERSIST ? 2 : 1) void eval_mfma_kernel(
                     if (p == ktile) {
                         group_end();
                         p = 0;
-                        ++g;
                     }
                 }
                 if (tt < tn) {
@@ -804,7 +829,6 @@ __global__ __launch_bounds__(WAVES * 64, PERSIST ? 2 : 1) void eval_mfma_kernel(
                     if (++p == ktile) {
                         group_end();
                         p = 0;
-                        ++g;
                     }
                 }
             }
@@ -816,7 +840,6 @@ __global__ __launch_bounds__(WAVES * 64, PERSIST ? 2 : 1) void eval_mfma_kernel(
                 if (++p == ktile) {
                     group_end();
                     p = 0;
-                    ++g;
                 }
             }
         }
@@ -923,8 +946,9 @@ hipError_t eval_launch_t(const MfmaArgs &x, hipStream_t st) {
     constexpr int NF = NKB * NB;
     constexpr int TB = tile_bytes_of(hdr_bytes(TILE, NB, splat_bias((int)sizeof(T), TILE, NKB)),
                                      HALF ? (NKB - 1) * NB : NF, HALF ? NB : 0);
-    constexpr int SB = stage_bytes<TB, NF, WAVES>();
-    constexpr int NBUF = ring_depth<TB, NF, WAVES>();
+    constexpr bool FILL = WAVES >= 8 && NB == 2;
+    constexpr int SB = stage_bytes<TB, NF, WAVES, FILL>();
+    constexpr int NBUF = ring_depth<TB, NF, WAVES, FILL>();
     auto kern = eval_mfma_kernel<T, TILE, NKB, NKS_LAST, RT, WAVES, MODE, HAS_M0, HALF, false>;
     auto kernp = eval_mfma_kernel<T, TILE, NKB, NKS_LAST, RT, WAVES, MODE, HAS_M0, HALF, MODE == MODE_SUM>;
     const size_t lds = (size_t)NBUF * SB;
@@ -998,6 +1022,9 @@ constexpr int plan_rt(int elem_bytes, int tile, int nkb) {
 }
 
 constexpr int plan_waves(int elem_bytes, int tile, int nkb) {
+    if (elem_bytes == 2 && tile == 16 && nkb >= EXEMCL_WIDE16_MIN_NKB) return EXEMCL_BIG_WAVES;
+    if (elem_bytes == 2 && tile == 16 && nkb >= EXEMCL_W12_MIN_NKB) return 12;
+    if (elem_bytes == 2 && tile == 16 && nkb <= EXEMCL_W16_MAX_NKB) return 16;
     if (nkb <= EXEMCL_BIG_NKB) return EXEMCL_SMALL_WAVES;
     return (elem_bytes == 2 && tile == 32 && nkb > 16) ? EXEMCL_WAVES16_BIG : EXEMCL_BIG_WAVES;
 }
