@@ -497,7 +497,9 @@ __global__ __launch_bounds__(WAVES * 64, PERSIST ? 2 : 1) void eval_mfma_kernel(
     // where they would hold registers through every MFMA chain.
     int tid = threadIdx.x, ldv = ld;
     if constexpr (PERSIST) asm volatile("" : "+v"(tid), "+s"(ldv));
-    const int lane = tid & 63, wave = tid >> 6;
+    // The wavefront index is uniform: held in a scalar register, so the LDS
+    // destination of every stage copy is scalar arithmetic (M0) too.
+    const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int lr = lane % TM, grp = lane / TM;
     const int64_t row0 = rb * (int64_t)(WAVES * RT * TM) + (int64_t)wave * RT * TM;
 
