@@ -335,9 +335,11 @@ bool rows_as_is(int precision, int64_t d) {
     return mfma_plan(precision, d, &mp) && mp.il && mp.nkb == 1;
 }
 
+// Temporary bytes of the padded copy of V (0 when rows of this d are read in
+// place; V whose alignment does not allow it is still copied).
 int64_t pad_bytes(int precision, int64_t n, int64_t d) {
-    if (rows_as_is(precision, d)) return 0;
-    return (d * elem_size(precision)) % 16 == 0 ? 0 : align_up(n * mfma_row_stride(precision, d) * elem_size(precision), 256);
+    if (rows_as_is(precision, d) || mfma_rows_in_place(precision, d)) return 0;
+    return align_up(n * mfma_row_stride(precision, d) * elem_size(precision), 256);
 }
 
 int prepare_rows(const void *V, int64_t n, int64_t d, int precision, hipStream_t st, MfmaRows *r,

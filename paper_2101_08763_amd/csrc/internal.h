@@ -69,10 +69,13 @@ struct ValuPlan {
 
 bool valu_plan(int prec, int64_t d, int64_t k, ValuPlan *p);
 
-// The MFMA kernels read V as rows of `ld` elements that are whole 16-byte
-// lane vectors: V 16-byte aligned, ld * element size a multiple of 16, zero
-// past the data's own d (mfma_row_stride, launch_pad).
+// The MFMA kernels read V as rows of `ld` elements whose lane vectors are
+// wholly inside a row or wholly past its data (zero there).  V can be read in
+// place (ld = d) when mfma_rows_in_place(prec, d) and V is aligned as
+// mfma_rows_ready checks; otherwise a zero-padded copy with row stride
+// mfma_row_stride (whole 16-byte vectors) is made (launch_pad).
 int64_t mfma_row_stride(int prec, int64_t d);
+bool mfma_rows_in_place(int prec, int64_t d);
 bool mfma_rows_ready(int prec, const void *V, int64_t d);
 
 // Vp[i][t] = V[i][t] for t < d, 0 for d <= t < ld (n rows).

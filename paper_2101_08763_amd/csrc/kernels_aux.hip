@@ -248,9 +248,25 @@ int64_t mfma_row_stride(int prec, int64_t d) {
     return (d + vec - 1) / vec * vec;
 }
 
+// Rows of d elements that the MFMA kernels (and the exemplar staging) can
+// read in place, with row stride d: every lane vector of a row lies wholly
+// inside the row or wholly past its end (those read as zeros), which holds
+// when d is a whole number of lane vectors -- or, for fp16/bf16 plans whose
+// last k-block is a half one (8-byte lane vectors of 4 coordinates after
+// whole 32-coordinate blocks), when d is a multiple of 4 (d = 100: 3 x 32
+// coordinates, then 4 of the half block).  fp32 rows must start 16-byte
+// aligned, fp16/bf16 rows 8-byte aligned (a 16-byte lane vector then sits
+// at an 8-byte aligned address; the loads need 4-byte alignment).
+bool mfma_rows_in_place(int prec, int64_t d) {
+    MfmaPlan pl;
+    if (!mfma_plan(prec, d, &pl)) return false;
+    if (prec == P_FP32) return d % 4 == 0;
+    return d % 8 == 0 || (pl.half && d % 4 == 0);
+}
+
 bool mfma_rows_ready(int prec, const void *V, int64_t d) {
-    const int64_t es = prec == P_FP32 ? 4 : 2;
-    return (uintptr_t)V % 16 == 0 && (d * es) % 16 == 0;
+    const uintptr_t align = prec == P_FP32 ? 16 : 8;
+    return mfma_rows_in_place(prec, d) && (uintptr_t)V % align == 0;
 }
 
 template <typename T>

@@ -273,11 +273,14 @@ def test_edge_cases(torch_gpu, orc):
 
 
 @pytest.mark.parametrize("prec,d", [("fp32", 2), ("fp32", 5), ("fp32", 8), ("fp32", 32), ("fp32", 100),
-                                    ("fp16", 12), ("bf16", 64)])
+                                    ("fp16", 12), ("bf16", 64), ("fp16", 100), ("bf16", 100), ("fp16", 36),
+                                    ("fp16", 164), ("bf16", 104)])
 def test_rows_at_any_alignment(torch_gpu, orc, prec, d):
     """V given as a view starting one element into its storage (4- or 2-byte
     aligned): rows read as they are (fp32, d <= 8) or through the padded
-    copy must give the same results as aligned V."""
+    copy must give the same results as aligned V -- which fp16/bf16 rows of
+    d = 36, 100, 164 (a half last k-block) and 104 read in place, without a
+    padded copy."""
     torch = torch_gpu
     n = 2001
     p = synth.random_problem(n + 1, d, 37, 6, seed=600 + d, clusters=3)
