@@ -149,6 +149,7 @@ def cpu_baseline(p: synth.Problem, X64: np.ndarray, budget_s: float):
 KERNEL_FILES = {
     "eval_mfma_kernel": ["device.hpp", "internal.h", "kernels_mfma.hip", "kernels_mfma_bf16.hip",
                          "kernels_mfma_f16.hip", "kernels_mfma_f32.hip", "mfma_kernels.hpp"],
+    "eval_bigd_kernel": ["bigd_kernels.hpp", "device.hpp", "internal.h", "kernels_mfma.hip", "kernels_mfma_bigd.hip"],
     "eval_valu_kernel": ["device.hpp", "internal.h", "kernels_aux.hip"],
     "sqnorm_kernel": ["device.hpp", "internal.h", "kernels_sqnorm.hip"],
 }
@@ -165,7 +166,7 @@ def kernel_source_hash(kernel: str = "eval_mfma_kernel") -> str:
             h.update(f.encode())
             h.update(fh.read())
     flags = [x for x in B.FLAGS if not x.startswith("-I")]
-    if kernel == "eval_mfma_kernel":
+    if kernel in ("eval_mfma_kernel", "eval_bigd_kernel"):
         flags += B.MFMA_FLAGS
     h.update(" ".join([B.ARCH] + flags).encode())
     return h.hexdigest()

@@ -97,7 +97,8 @@ enum exemcl_path {
  *
  *   V          device, n x d row-major, type per `precision`; read only
  *   n          number of ground points, 1 <= n <= INT32_MAX
- *   d          dimension, 1 <= d <= 512 (larger d: EINVAL in this version)
+ *   d          dimension, 1 <= d <= 2^24 (rows are addressed through 32-bit
+ *              byte offsets per block of 32 points)
  *   sets       device, l x k int32 row-major; read only (may be NULL if k == 0)
  *   l          number of sets, l >= 0 (l == 0: returns EXEMCL_OK, queues nothing)
  *   k          set size, k >= 0 (k == 0: every out[j] = 0, since f(empty) = 0)
@@ -106,7 +107,7 @@ enum exemcl_path {
  *   stream     hipStream_t or NULL
  *
  * Errors: EINVAL for a NULL array with a non-zero size, n < 1, n > INT32_MAX,
- * d < 1, d > 512, k < 0, l < 0 or an unknown precision; EDEVICE when a
+ * d < 1, d > 2^24, k < 0, l < 0 or an unknown precision; EDEVICE when a
  * launch fails.  Temporary buffers (partial sums and staged exemplar tiles,
  * O(l*k*d) bytes) come from the library's pool; when the whole batch does not
  * fit (or exceeds EXEMCL_WORKSPACE_LIMIT bytes), the batch is processed in
@@ -239,7 +240,7 @@ EXEMCL_API int exemplar_gain(const float *V, int64_t n, int64_t d, const int32_t
  * (bitwise), so f_out[i] - f_out[i-1] is the round's discrete derivative
  * (Definition 1).  Temporary memory: about 17 bytes per point plus a scoring
  * workspace kept under 1 GiB by scoring the candidates in chunks.
- * Errors: EINVAL for bad sizes (K > n, d > 512) or NULL outputs when K > 0;
+ * Errors: EINVAL for bad sizes (K > n, d > 2^24) or NULL outputs when K > 0;
  * ENOMEM / EDEVICE as for exemplar_eval.
  */
 EXEMCL_API int exemplar_greedy(const float *V, int64_t n, int64_t d, int64_t K, int32_t *S_out,

@@ -21,7 +21,8 @@ HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
 SOURCES = ["host.cpp", "kernels_mfma.hip", "kernels_mfma_f32.hip", "kernels_mfma_f16.hip",
-           "kernels_mfma_bf16.hip", "kernels_aux.hip", "kernels_greedy.hip", "kernels_sqnorm.hip"]
+           "kernels_mfma_bf16.hip", "kernels_mfma_bigd.hip", "kernels_aux.hip", "kernels_greedy.hip",
+           "kernels_sqnorm.hip"]
 FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-fvisibility=hidden",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
          "-Wall", "-Wno-unused-result", f"-I{INCLUDE}", f"-I{CSRC}"]

@@ -27,6 +27,9 @@ struct MfmaPlan {
     int half;       // 1: the last k-block holds 16 coordinates (16x16x16 instruction)
     int splat;      // 1: tile headers hold bf16 bias parts for the splat MFMA (32-column tiles, few k-blocks)
     int il;         // 1: fp32 single k-block with coordinates 2e + g (ceil(d/2) instructions; rows need no padding)
+    int bigd;       // 1: d > 512, the coordinates split over the wavefronts (bigd_kernels.hpp)
+    int kw;         // bigd: k-blocks per wavefront and round (a compiled bucket: 2, 4, 8)
+    int rounds;     // bigd: rounds of 8 * kw k-blocks that cover d
 };
 
 bool mfma_plan(int prec, int64_t d, MfmaPlan *p);
@@ -57,6 +60,8 @@ hipError_t pack_run_bf16(const MfmaPlan &pl, const void *V, int64_t n, int ld, c
 hipError_t eval_run_f32(const MfmaPlan &pl, int mode, const MfmaArgs &x, hipStream_t st);
 hipError_t eval_run_f16(const MfmaPlan &pl, int mode, const MfmaArgs &x, hipStream_t st);
 hipError_t eval_run_bf16(const MfmaPlan &pl, int mode, const MfmaArgs &x, hipStream_t st);
+// The d > 512 kernel (kernels_mfma_bigd.hip), every storage type.
+hipError_t bigd_run(int prec, int mode, const MfmaPlan &pl, const MfmaArgs &x, hipStream_t st);
 
 // Geometry of one VALU evaluation launch.
 struct ValuPlan {

@@ -17,6 +17,9 @@
 #ifndef EXEMCL_HALF_MAX_D
 #define EXEMCL_HALF_MAX_D 192
 #endif
+#ifndef EXEMCL_MAIN_MAX_D16
+#define EXEMCL_MAIN_MAX_D16 1024
+#endif
 #if EXEMCL_HALF_MAX_D > 192
 #error "half k-blocks are compiled for 2 to 6 k-blocks (d <= 192)"
 #endif
@@ -32,9 +35,37 @@ static int bucket(int nkb) {
     return -1;
 }
 
+// Largest d: the kernels address a block of rows through 32-bit byte
+// offsets (32 rows of at most 2^24 fp32 coordinates).
+constexpr int64_t kMaxD = int64_t(1) << 24;
+
 bool mfma_plan(int prec, int64_t d, MfmaPlan *p) {
-    if (d < 1 || d > 512) return false;
+    if (d < 1 || d > kMaxD) return false;
     MfmaPlan q{};
+    // fp16/bf16 up to d = 1024 stay on the register-resident kernel (one row
+    // tile of 16 points and 32 k-blocks per wavefront); above that, and fp32
+    // above 512, the coordinates are split over the wavefronts.
+    const int64_t dmax_main = (prec == P_FP32) ? 512 : EXEMCL_MAIN_MAX_D16;
+    if (d > dmax_main) {
+        // Coordinates split over the 8 wavefronts of a workgroup sharing 32
+        // points: 16x16x4 (fp32, 16 coordinates per k-block) or 16x16x32
+        // (fp16/bf16, 32 per k-block, two members per tile); each wavefront
+        // holds kw k-blocks per round, and d needs `rounds` rounds.
+        q.bigd = 1;
+        q.tile = 16;
+        q.nb = prec == P_FP32 ? 1 : EXEMCL_NB16;
+        q.kb_dims = prec == P_FP32 ? 16 : 32;
+        q.nkb = (int)((d + q.kb_dims - 1) / q.kb_dims);
+        q.nks_last = prec == P_FP32 ? 4 : 1;
+        const int per = (q.nkb + 7) / 8;
+        q.kw = per <= 2 ? 2 : per <= 4 ? 4 : 8;
+        q.rounds = (q.nkb + 8 * q.kw - 1) / (8 * q.kw);
+        q.rt = 2;
+        q.waves = 8;
+        q.rows = 32;
+        *p = q;
+        return true;
+    }
     q.waves = 4;
     q.nb = 1;
     q.half = 0;
@@ -111,6 +142,7 @@ hipError_t launch_mfma(int prec, int mode, const MfmaPlan &pl, const void *V, in
                        int64_t kt, int64_t ngroups, int64_t gpc, const float *m0, float *partials, int64_t lpad,
                        float *rowmax, hipStream_t st, hipEvent_t ev_start, hipEvent_t ev_stop) {
     const MfmaArgs x{V, n, ld, tiles, kt, ngroups, gpc, m0, partials, lpad, rowmax, ev_start, ev_stop};
+    if (pl.bigd) return bigd_run(prec, mode, pl, x, st);
     switch (prec) {
     case P_FP32: return eval_run_f32(pl, mode, x, st);
     case P_FP16: return mode == MODE_SUM ? eval_run_f16(pl, mode, x, st) : hipErrorInvalidValue;

@@ -1018,7 +1018,11 @@ hipError_t eval_launch(const MfmaArgs &x, hipStream_t st) {
 // as functions of (element bytes, tile, k-blocks) so that the host-side plan
 // (mfma_plan) and the compiled instantiations follow one rule.
 constexpr int plan_rt(int elem_bytes, int tile, int nkb) {
-    if (tile == 16) return elem_bytes == 4 ? 1 : nkb <= EXEMCL_RT16X16_NKB ? EXEMCL_RT16X16_SMALL : EXEMCL_RT16X16_BIG;
+    if (tile == 16)
+        return elem_bytes == 4            ? 1
+               : nkb <= EXEMCL_RT16X16_NKB ? EXEMCL_RT16X16_SMALL
+               : nkb <= 16                 ? EXEMCL_RT16X16_BIG
+                                           : 1;  // 512 < d <= 1024: one row tile of 32 k-blocks
     if (elem_bytes == 4) return nkb <= EXEMCL_RT1_NKB32 ? 1 : nkb <= 16 ? 2 : 1;
     return nkb <= EXEMCL_BIG_NKB ? EXEMCL_RT16_SMALL : nkb <= 16 ? EXEMCL_RT16_MID : EXEMCL_RT16_BIG;
 }
@@ -1125,9 +1129,9 @@ hipError_t eval_dispatch(const MfmaPlan &pl, const MfmaArgs &x, hipStream_t st) 
         case 14: return eval_launch<T, TILE, 14, KL, rt_of<T, TILE, 14>(), waves_of<T, TILE, 14>(), MODE>(x, st);
         case 16: return eval_launch<T, TILE, 16, KL, rt_of<T, TILE, 16>(), waves_of<T, TILE, 16>(), MODE>(x, st);
         }
-        // 16 k-blocks of 32 coordinates already cover d = 512 for the
-        // 16x16x32 shape; the 16- and 8-coordinate shapes need more.
-        if constexpr (Mfma<T, TILE>::KB_DIMS < 32) {
+        // The 16x16x32 shape reaches d = 1024 with 32 k-blocks (one row
+        // tile per wavefront); the 16- and 8-coordinate shapes reach 512.
+        {
             switch (pl.nkb) {
             case 20: return eval_launch<T, TILE, 20, KL, rt_of<T, TILE, 20>(), waves_of<T, TILE, 20>(), MODE>(x, st);
             case 24: return eval_launch<T, TILE, 24, KL, rt_of<T, TILE, 24>(), waves_of<T, TILE, 24>(), MODE>(x, st);

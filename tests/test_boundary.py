@@ -56,10 +56,16 @@ def test_eval_rejects(lib, bad):
 
 
 def test_eval_dimension_limit(lib):
-    rc = lib.exemplar_eval(FAKE, 100, 513, FAKE, 4, 3, 0, FAKE, None)
+    """Any d up to 2^24 has a plan (above 512 the coordinates are split over
+    the wavefronts of a workgroup); larger rows exceed the kernels' 32-bit
+    row-window offsets and are refused before anything is queued."""
+    for d in (512, 513, 1000, 2048, 4100, 1 << 24):
+        for prec in (api.EXEMCL_FP32, api.EXEMCL_FP16, api.EXEMCL_BF16):
+            assert api.exemplar_plan(100, d, 4, 3, prec)[0] == "mfma"
+    rc = lib.exemplar_eval(FAKE, 100, (1 << 24) + 1, FAKE, 4, 3, 0, FAKE, None)
     assert rc == api.EXEMCL_EINVAL
     with pytest.raises(api.ExemclError):
-        api.exemplar_plan(100, 513, 4, 3)
+        api.exemplar_plan(100, (1 << 24) + 1, 4, 3)
 
 
 def test_eval_empty_batch_is_a_noop(lib):
@@ -78,7 +84,7 @@ def test_gain_rejects(lib, bad):
     assert rc == api.EXEMCL_EINVAL
 
 
-BAD_GREEDY = [dict(V=None), dict(n=0), dict(n=2**31), dict(d=0), dict(d=513), dict(K=-1), dict(K=101),
+BAD_GREEDY = [dict(V=None), dict(n=0), dict(n=2**31), dict(d=0), dict(d=(1 << 24) + 1), dict(K=-1), dict(K=101),
               dict(S=None), dict(f=None)]
 
 
@@ -140,7 +146,7 @@ def test_workspace_is_bounded():
 
 # exemplar_eval_streamed takes host arrays: its argument checks and the k = 0
 # case (f(empty) = 0, written on the host) run without a device.
-BAD_STREAMED = BAD_EVAL + [dict(rows_per_block=-1), dict(d=513)]
+BAD_STREAMED = BAD_EVAL + [dict(rows_per_block=-1), dict(d=(1 << 24) + 1)]
 
 
 @pytest.mark.parametrize("bad", BAD_STREAMED, ids=[str(b) for b in BAD_STREAMED])

@@ -241,6 +241,76 @@ def test_large1m_sampled(torch_gpu, large1m_ref):
 
 
 # ---------------------------------------------------------------------------
+# Dimensions above 512.  fp16/bf16 up to 1024 run the register-resident
+# kernel with one row tile per wavefront (513, 1000); fp32 above 512 and
+# fp16/bf16 above 1024 split the coordinates over the wavefronts of a
+# workgroup and add the partial products in LDS, with one round of
+# register-held points (fp32 <= 1024, fp16/bf16 <= 2048) or several (the
+# points reloaded per tile batch: 2048 and 4100 fp32, 4100 fp16/bf16).
+# Ragged n, k and l.
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("prec", ["fp32", "fp16", "bf16"])
+@pytest.mark.parametrize("d", [513, 1000, 1025, 2048, 4100])
+def test_large_d(torch_gpu, orc, prec, d):
+    n, l, k = 1037 if d <= 2048 else 333, 37, 5
+    p = synth.random_problem(n, d, l, k, seed=4000 + d, clusters=3)
+    say(f"large d prec={prec} n={n} d={d} l={l} k={k}")
+    Vg, X64 = to_gpu(torch_gpu, p.X, prec)
+    got = gpu_eval(torch_gpu, Vg, p.sets)
+    want = orc.eval(X64, p.sets, 8)
+    check(got, want, orc.loss_e0(X64), prec, f"d={d}")
+    exact(got, want, f"{prec} d={d}")
+
+
+def test_large_d_batch_independence_and_edges(torch_gpu, orc):
+    torch = torch_gpu
+    d = 1000
+    p = synth.random_problem(900, d, 50, 6, seed=4500, clusters=2)
+    Vg, X64 = to_gpu(torch, p.X, "fp16")
+    a = gpu_eval(torch, Vg, p.sets)
+    perm = np.random.default_rng(1).permutation(50)
+    assert np.array_equal(a[perm], gpu_eval(torch, Vg, p.sets[perm])), "batch position"
+    assert np.array_equal(a[7:8], gpu_eval(torch, Vg, p.sets[7:8])), "batch size 1"
+    sets = p.sets[:6].copy()
+    sets[1, 3:] = -1          # shorter set
+    sets[2, :] = -1           # all empty: 0
+    sets[3, 0] = 900          # invalid: NaN
+    got = gpu_eval(torch, Vg, sets)
+    want = orc.eval(X64, sets, 8)
+    assert got[2] == 0.0 and np.isnan(got[3])
+    check(got, want, orc.loss_e0(X64), "fp16", "large d edge cases")
+
+
+@pytest.mark.parametrize("d", [700, 1100])
+def test_large_d_gain_and_greedy(torch_gpu, orc, d):
+    """exemplar_gain (the per-point cache, then the scoring of S u {c}) and
+    two greedy rounds at d > 512, fp32."""
+    torch = torch_gpu
+    n = 1500
+    p = synth.random_problem(n, d, 1, 1, seed=4600 + d, clusters=4)
+    rng = np.random.default_rng(d)
+    S = rng.choice(n, 21, replace=False).astype(np.int32)
+    cands = np.concatenate([rng.choice(n, 40, replace=False), S[:2]]).astype(np.int32)
+    Vg, X64 = to_gpu(torch, p.X, "fp32")
+    got = api.exemplar_gain(Vg, torch.from_numpy(S).cuda(), torch.from_numpy(cands).cuda())
+    torch.cuda.synchronize()
+    got = got.cpu().numpy().astype(np.float64)
+    le0 = orc.loss_e0(X64)
+    want = orc.gain(X64, S, cands, 8)
+    check(got, want, le0, "fp32", f"gain d={d}")
+    exact(got, want, f"gain d={d}")
+    gS, gf = api.exemplar_greedy(Vg, 2)
+    torch.cuda.synchronize()
+    gS, gf = gS.cpu().numpy(), gf.cpu().numpy().astype(np.float64)
+    for i in range(2):
+        rest = np.setdiff1d(np.arange(n), gS[:i]).astype(np.int32)
+        sc = orc.gain(X64, gS[:i], rest, 8)
+        mine = sc[np.searchsorted(rest, gS[i])]
+        tol = 1e-5 * abs(sc.max()) + 1e-7 * le0
+        assert mine >= sc.max() - 2 * tol and abs(gf[i] - mine) <= tol, f"greedy round {i}"
+
+
+# ---------------------------------------------------------------------------
 # Edge cases.
 # ---------------------------------------------------------------------------
 def test_edge_cases(torch_gpu, orc):

@@ -45,7 +45,7 @@ def streamed(V, S, rows):
 # Several blocks with a ragged last one, every storage type, dimensions with
 # and without padded rows (and a half last k-block for fp16/bf16 at d = 100).
 @pytest.mark.parametrize("prec", ["fp32", "fp16", "bf16"])
-@pytest.mark.parametrize("d", [8, 33, 100, 128])
+@pytest.mark.parametrize("d", [8, 33, 100, 128, 600])
 def test_streamed_matches_oracle(torch_gpu, orc, prec, d):
     torch = torch_gpu
     n, l, k = 5003, 70, 7
