@@ -32,6 +32,13 @@
  *   - V is dense row-major n x d (row stride d elements, no padding), with
  *     element type fp32, fp16 or bf16 as selected by `precision`.  Results are
  *     fp32.  Arithmetic is fp32 (fp16/bf16 products are exact in fp32).
+ *   - V must hold finite values.  The kernels' maxima are compiled without
+ *     NaN semantics, so a NaN or infinity anywhere in V gives unspecified
+ *     results for every set (no error is reported and nothing faults); it
+ *     is not detected.  (f itself would be NaN or infinite there.)  The
+ *     sums of squares must also stay finite in fp32, which holds for any
+ *     finite fp16 data (d <= 2^24) and for fp32 and bf16 data below about
+ *     1.8e19 / sqrt(d) in magnitude.
  *   - Sets are int32 row indices into V.  Duplicate indices are allowed.
  *     EXEMCL_EMPTY_SLOT (-1) marks an empty slot, so sets of different sizes
  *     share one k (the blank fields of the paper's evaluation-set matrix,
