@@ -86,7 +86,9 @@ bool layout_eval(int64_t n, int64_t d, int64_t l, int64_t k, int precision, int 
         L->ngroups = (l + tm - 1) / tm;
         L->lpad = L->ngroups * tm;
         const int64_t nrb = (n + L->mp.rows - 1) / L->mp.rows;
-        L->G = nrb * L->mp.waves;  // one partial-sum row per wavefront
+        // one partial-sum row per wavefront, or per workgroup when the kernel
+        // adds its wavefronts' sums itself
+        L->G = nrb * (L->mp.wgsum ? 1 : L->mp.waves);
         const int64_t target = wg_target();
         int64_t chunks = (target + nrb - 1) / nrb;
         if (chunks < 1) chunks = 1;

@@ -27,6 +27,7 @@ struct MfmaPlan {
     int half;       // 1: the last k-block holds 16 coordinates (16x16x16 instruction)
     int splat;      // 1: tile headers hold bf16 bias parts for the splat MFMA (32-column tiles, few k-blocks)
     int il;         // 1: fp32 single k-block with coordinates 2e + g (ceil(d/2) instructions; rows need no padding)
+    int wgsum;      // 1: the kernel adds its wavefronts' partial sums: one partial-sum row per row block
     int bigd;       // 1: d > 512, the coordinates split over the wavefronts (bigd_kernels.hpp)
     int kw;         // bigd: k-blocks per wavefront and round (a compiled bucket: 2, 4, 8)
     int rounds;     // bigd: rounds of 8 * kw k-blocks that cover d

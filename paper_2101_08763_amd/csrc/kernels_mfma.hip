@@ -117,6 +117,7 @@ bool mfma_plan(int prec, int64_t d, MfmaPlan *p) {
     q.waves = plan_waves(eb, q.tile, q.nkb);
     q.rows = q.waves * q.rt * q.tile;
     q.splat = splat_bias(eb, q.tile, q.nkb) ? 1 : 0;
+    q.wgsum = wg_sum(q.waves, q.nb) ? 1 : 0;
     *p = q;
     return true;
 }

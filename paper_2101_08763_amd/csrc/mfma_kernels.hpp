@@ -352,6 +352,13 @@ constexpr int lds_budget() {
     return WAVES <= 4 ? kLdsBytes / 2 : kLdsBytes;
 }
 
+// One-workgroup-per-CU plans (8 or more wavefronts, two members per tile:
+// FILL below) add their wavefronts' partial sums in LDS at each set group's
+// end and store one partial-sum row per workgroup; the host sizes the
+// partial sums with the same rule.  kWgSumLds bytes of LDS are kept for it.
+constexpr bool wg_sum(int waves, int nb) { return waves >= 8 && nb == 2; }
+constexpr int kWgSumLds = 4096;
+
 // Stage geometry for tiles of TB bytes and NFRAG B fragments.  FILL (8
 // wavefronts, two-member tiles: one workgroup per CU in lockstep) takes as
 // many tiles per stage as two stages fit in the LDS, since the cost of a
@@ -360,7 +367,8 @@ template <int TB, int NFRAG, int WAVES, bool FILL = false>
 constexpr int tiles_per_stage() {
     int tps = FILL ? EXEMCL_TPS_FILL_MAX
                    : NFRAG <= EXEMCL_BIG_NKB ? (EXEMCL_STAGE_MIN / TB > 1 ? EXEMCL_STAGE_MIN / TB : 1) : EXEMCL_TPS_BIG;
-    while (tps > 1 && 2 * round_stage<NFRAG, WAVES>(tps * TB) > lds_budget<WAVES>()) --tps;
+    constexpr int budget = FILL ? kLdsBytes - kWgSumLds : lds_budget<WAVES>();
+    while (tps > 1 && 2 * round_stage<NFRAG, WAVES>(tps * TB) > budget) --tps;
     return tps;
 }
 
@@ -455,11 +463,16 @@ __global__ __launch_bounds__(WAVES * 64, PERSIST ? 2 : 1) void eval_mfma_kernel(
     constexpr int NBIAS = SPLAT ? 2 : NB;  // bias registers per tile (SPLAT: the 8 header bytes)
     constexpr int HDR = hdr_bytes(TM, NB, SPLAT);
     constexpr int TB = tile_bytes_of(HDR, NFF, HALF ? NB : 0);
-    constexpr bool FILL = WAVES >= 8 && NB == 2;
+    constexpr bool FILL = wg_sum(WAVES, NB);
     constexpr int SB = stage_bytes<TB, NF, WAVES, FILL>();
     constexpr int TPS = tiles_per_stage<TB, NF, WAVES, FILL>();
     constexpr int CNT = SB / (NT * 16);
     constexpr int NBUF = ring_depth<TB, NF, WAVES, FILL>();
+    // Wavefront partial sums added in LDS per set group (wg_sum): two
+    // buffers of WAVES x TM floats after the stage ring, by group parity.
+    constexpr bool WGSUM = FILL && MODE == MODE_SUM;
+    static_assert(!WGSUM || 2 * WAVES * TM * 4 <= kWgSumLds, "partial-sum buffers");
+    static_assert(!FILL || NBUF * SB + kWgSumLds <= kLdsBytes, "LDS");
     static_assert(!HALF || (M::HAS_HALF && NKB >= 2), "half k-block needs the 16x16x16 instruction and a whole block");
     // Reads across tiles pay off for long tiles; short ones keep the registers
     // for a third wavefront per SIMD instead.
@@ -728,7 +741,7 @@ __global__ __launch_bounds__(WAVES * 64, PERSIST ? 2 : 1) void eval_mfma_kernel(
     // partial-sum row of fp32 values); keeping them 32-bit keeps them in
     // scalar registers.
     const int ktile = (int)kt;
-    float *wpart = partials + (rb * WAVES + wave) * lpad;
+    float *wpart = partials + (WGSUM ? rb : rb * WAVES + wave) * lpad;
     int g = (int)g0;
     int p = 0;
     const int nst = (int)nstages;
@@ -740,7 +753,22 @@ __global__ __launch_bounds__(WAVES * 64, PERSIST ? 2 : 1) void eval_mfma_kernel(
             float sum = lane_sum();
 #pragma unroll
             for (int off = TM; off < 64; off <<= 1) sum += __shfl_xor(sum, off);
-            if (grp == 0) wpart[(int64_t)g * TM + lr] = sum;
+            if constexpr (WGSUM) {
+                // every wavefront of the workgroup ends group g here: add
+                // their sums in wavefront order and store one row (the next
+                // group's barrier separates reuse of a parity's buffer)
+                float *red = reinterpret_cast<float *>(smem + NBUF * SB) + (g & 1) * (WAVES * TM);
+                if (grp == 0) red[wave * TM + lr] = sum;
+                __syncthreads();
+                if (wave == 0 && grp == 0) {
+                    float t = red[lr];
+#pragma unroll
+                    for (int w = 1; w < WAVES; ++w) t += red[w * TM + lr];
+                    wpart[(int64_t)g * TM + lr] = t;
+                }
+            } else {
+                if (grp == 0) wpart[(int64_t)g * TM + lr] = sum;
+            }
 #pragma unroll
             for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
@@ -948,12 +976,12 @@ hipError_t eval_launch_t(const MfmaArgs &x, hipStream_t st) {
     constexpr int NF = NKB * NB;
     constexpr int TB = tile_bytes_of(hdr_bytes(TILE, NB, splat_bias((int)sizeof(T), TILE, NKB)),
                                      HALF ? (NKB - 1) * NB : NF, HALF ? NB : 0);
-    constexpr bool FILL = WAVES >= 8 && NB == 2;
+    constexpr bool FILL = wg_sum(WAVES, NB);
     constexpr int SB = stage_bytes<TB, NF, WAVES, FILL>();
     constexpr int NBUF = ring_depth<TB, NF, WAVES, FILL>();
     auto kern = eval_mfma_kernel<T, TILE, NKB, NKS_LAST, RT, WAVES, MODE, HAS_M0, HALF, false>;
     auto kernp = eval_mfma_kernel<T, TILE, NKB, NKS_LAST, RT, WAVES, MODE, HAS_M0, HALF, MODE == MODE_SUM>;
-    const size_t lds = (size_t)NBUF * SB;
+    const size_t lds = (size_t)NBUF * SB + (FILL && MODE == MODE_SUM ? kWgSumLds : 0);
     if (lds > 64 * 1024) {
         hipError_t e = hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
         if (e == hipSuccess && MODE == MODE_SUM)
