@@ -326,6 +326,23 @@ __global__ __launch_bounds__(64) void pack_tiles_kernel(const T *__restrict__ V,
 #ifndef EXEMCL_WIDE16_MIN_NKB
 #define EXEMCL_WIDE16_MIN_NKB 6
 #endif
+#ifndef EXEMCL_WIDE16_WAVES
+#define EXEMCL_WIDE16_WAVES 8
+#endif
+// Up to 8 k-blocks these plans take as many row tiles per wavefront as fit
+// EXEMCL_WIDE16_A_BLOCKS A fragments (4 VGPRs each: 160 of the 256), at most
+// EXEMCL_RT_WIDE16_MAX: every B fragment read from LDS then feeds 5-6 MFMAs.
+// Their cross-tile reads keep EXEMCL_PF_WIDE16 fragments in flight, which
+// leaves the registers for the fifth row tile.
+#ifndef EXEMCL_WIDE16_A_BLOCKS
+#define EXEMCL_WIDE16_A_BLOCKS 40
+#endif
+#ifndef EXEMCL_RT_WIDE16_MAX
+#define EXEMCL_RT_WIDE16_MAX 6
+#endif
+#ifndef EXEMCL_PF_WIDE16
+#define EXEMCL_PF_WIDE16 2
+#endif
 // Shorter two-member tiles (EXEMCL_W12_MIN_NKB .. EXEMCL_WIDE16_MIN_NKB - 1
 // k-blocks) fit three wavefronts per SIMD: one 12-wavefront workgroup per CU.
 #ifndef EXEMCL_W12_MIN_NKB
@@ -480,7 +497,8 @@ __global__ __launch_bounds__(WAVES * 64, PERSIST ? 2 : 1) void eval_mfma_kernel(
     // B fragments in flight ahead of use.  When the reads run across tiles
     // (SCHED) the ring of PF slots must wrap exactly at a tile's end, so PF
     // divides NF; the next tile then finds fragment i in slot i.
-    constexpr int PF = SCHED ? prefetch_depth(NF, EXEMCL_PF_SCHED) : (NFF < EXEMCL_PF ? NFF : EXEMCL_PF);
+    constexpr int PF = SCHED ? prefetch_depth(NF, FILL && NKB <= EXEMCL_RT16X16_NKB ? EXEMCL_PF_WIDE16 : EXEMCL_PF_SCHED)
+                             : (NFF < EXEMCL_PF ? NFF : EXEMCL_PF);
     static_assert(!SCHED || NF % PF == 0, "cross-tile prefetch ring must wrap at the tile end");
     static_assert(!SPLAT || (!SCHED && NB == 1 && !HALF), "splat tiles");
     static_assert(MODE == MODE_SUM || NB == 1, "the row-max mode stages one member per tile");
@@ -721,19 +739,22 @@ __global__ __launch_bounds__(WAVES * 64, PERSIST ? 2 : 1) void eval_mfma_kernel(
 #pragma unroll
             for (int i = 0; i < M::ACC; ++i) m[rt][i] = fmaxf(fmaxf(m[rt][i], x[rt][0][i]), y[rt][0][i]);
     };
-    // Sum of this lane's running maxima in a fixed pairwise order.
+    // Sum of this lane's running maxima in a fixed pairwise order: each level
+    // adds the upper ceil(n/2) values to the lower ones (for a power of two,
+    // halves).
     auto lane_sum = [&]() {
         constexpr int NV = RT * M::ACC;
-        static_assert((NV & (NV - 1)) == 0, "pairwise sum over a power of two");
         float v[NV];
 #pragma unroll
         for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
             for (int i = 0; i < M::ACC; ++i) v[rt * M::ACC + i] = m[rt][i];
 #pragma unroll
-        for (int w = NV / 2; w >= 1; w /= 2)
+        for (int n = NV; n > 1; n = (n + 1) / 2) {
+            const int h = (n + 1) / 2;
 #pragma unroll
-            for (int i = 0; i < w; ++i) v[i] += v[i + w];
+            for (int i = 0; i + h < n; ++i) v[i] += v[i + h];
+        }
         return v[0];
     };
 
@@ -1042,12 +1063,17 @@ hipError_t eval_launch(const MfmaArgs &x, hipStream_t st) {
     return eval_launch_t<T, TILE, NKB, NKS_LAST, RT, WAVES, MODE, false, HALF>(x, st);
 }
 
+constexpr int wide16_rt(int nkb) {
+    return EXEMCL_WIDE16_A_BLOCKS / nkb < EXEMCL_RT_WIDE16_MAX ? EXEMCL_WIDE16_A_BLOCKS / nkb : EXEMCL_RT_WIDE16_MAX;
+}
+
 // Row tiles per wavefront and wavefronts per workgroup for a k-block bucket,
 // as functions of (element bytes, tile, k-blocks) so that the host-side plan
 // (mfma_plan) and the compiled instantiations follow one rule.
 constexpr int plan_rt(int elem_bytes, int tile, int nkb) {
     if (tile == 16)
         return elem_bytes == 4            ? 1
+               : (nkb >= EXEMCL_WIDE16_MIN_NKB && nkb <= EXEMCL_RT16X16_NKB) ? wide16_rt(nkb)
                : nkb <= EXEMCL_RT16X16_NKB ? EXEMCL_RT16X16_SMALL
                : nkb <= 16                 ? EXEMCL_RT16X16_BIG
                                            : 1;  // 512 < d <= 1024: one row tile of 32 k-blocks
@@ -1056,6 +1082,7 @@ constexpr int plan_rt(int elem_bytes, int tile, int nkb) {
 }
 
 constexpr int plan_waves(int elem_bytes, int tile, int nkb) {
+    if (elem_bytes == 2 && tile == 16 && nkb >= EXEMCL_WIDE16_MIN_NKB && nkb <= EXEMCL_RT16X16_NKB) return EXEMCL_WIDE16_WAVES;
     if (elem_bytes == 2 && tile == 16 && nkb >= EXEMCL_WIDE16_MIN_NKB) return EXEMCL_BIG_WAVES;
     if (elem_bytes == 2 && tile == 16 && nkb >= EXEMCL_W12_MIN_NKB) return 12;
     if (elem_bytes == 2 && tile == 16 && nkb <= EXEMCL_W16_MAX_NKB) return 16;
