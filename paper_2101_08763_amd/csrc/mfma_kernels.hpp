@@ -280,8 +280,11 @@ __global__ __launch_bounds__(64) void pack_tiles_kernel(const T *__restrict__ V,
 #ifndef EXEMCL_BIG_WAVES
 #define EXEMCL_BIG_WAVES 8
 #endif
+// fp16/bf16 32x32x16 tiles (d <= 16): every tile's bias splat is one MFMA
+// shared by the wavefront's row tiles, a third of the matrix-core time with
+// 2 row tiles and a fifth with 4 (about 240 VGPRs: two wavefronts per SIMD).
 #ifndef EXEMCL_RT16_SMALL
-#define EXEMCL_RT16_SMALL 2
+#define EXEMCL_RT16_SMALL 4
 #endif
 #ifndef EXEMCL_RT16_MID
 #define EXEMCL_RT16_MID 2
