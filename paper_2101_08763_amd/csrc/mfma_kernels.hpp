@@ -244,6 +244,9 @@ __global__ __launch_bounds__(64) void pack_tiles_kernel(const T *__restrict__ V,
 #ifndef EXEMCL_PF_SCHED
 #define EXEMCL_PF_SCHED 4
 #endif
+#ifndef EXEMCL_PF_BIG3
+#define EXEMCL_PF_BIG3 2
+#endif
 #ifndef EXEMCL_PERSIST_DEFAULT
 #define EXEMCL_PERSIST_DEFAULT 1
 #endif
@@ -500,7 +503,9 @@ __global__ __launch_bounds__(WAVES * 64, PERSIST ? 2 : 1) void eval_mfma_kernel(
     // B fragments in flight ahead of use.  When the reads run across tiles
     // (SCHED) the ring of PF slots must wrap exactly at a tile's end, so PF
     // divides NF; the next tile then finds fragment i in slot i.
-    constexpr int PF = SCHED ? prefetch_depth(NF, FILL && NKB <= EXEMCL_RT16X16_NKB ? EXEMCL_PF_WIDE16 : EXEMCL_PF_SCHED)
+    constexpr int PF = SCHED ? prefetch_depth(NF, FILL && NKB <= EXEMCL_RT16X16_NKB ? EXEMCL_PF_WIDE16
+                                                  : FILL && RT >= 3                   ? EXEMCL_PF_BIG3
+                                                                                      : EXEMCL_PF_SCHED)
                              : (NFF < EXEMCL_PF ? NFF : EXEMCL_PF);
     static_assert(!SCHED || NF % PF == 0, "cross-tile prefetch ring must wrap at the tile end");
     static_assert(!SPLAT || (!SCHED && NB == 1 && !HALF), "splat tiles");
@@ -567,9 +572,9 @@ __global__ __launch_bounds__(WAVES * 64, PERSIST ? 2 : 1) void eval_mfma_kernel(
     using hvec_t = typename M::hvec_t;
     vec_t a[RT][NKF];
     hvec_t ah[HALF ? RT : 1];  // the half k-block's 8-byte lane vectors
-    // The workgroup's rows as one buffer window (at most 512 rows of at most
-    // 512 elements, so 32-bit offsets): rows past n read as zeros, and so do
-    // vectors past ld, without a branch.
+    // The workgroup's rows as one buffer window (at most 1 536 rows of at
+    // most 1 024 elements, so 32-bit offsets): rows past n read as zeros, and
+    // so do vectors past ld, without a branch.
     const int64_t wrow0 = rb * (int64_t)(WAVES * RT * TM);
     const int64_t wrows = min((int64_t)(WAVES * RT * TM), n - wrow0);
     const auto vwin = window_rsrc(V + wrow0 * (int64_t)ld, (uint32_t)(wrows * ld * (int64_t)sizeof(T)));
@@ -1070,6 +1075,28 @@ constexpr int wide16_rt(int nkb) {
     return EXEMCL_WIDE16_A_BLOCKS / nkb < EXEMCL_RT_WIDE16_MAX ? EXEMCL_WIDE16_A_BLOCKS / nkb : EXEMCL_RT_WIDE16_MAX;
 }
 
+// The 12-wavefront plans (168 VGPRs) take EXEMCL_W12_A_BLOCKS A fragments,
+// at least EXEMCL_RT16X16_SMALL and at most EXEMCL_RT_W12_MAX row tiles; the
+// 16-wavefront one (128 VGPRs) EXEMCL_RT16X16_W16; above 256 coordinates up
+// to EXEMCL_RT16X16_BIG3_NKB k-blocks take 3 row tiles (with EXEMCL_PF_BIG3
+// fragments in flight, which leaves the registers for them), the rest 2.
+#ifndef EXEMCL_W12_A_BLOCKS
+#define EXEMCL_W12_A_BLOCKS 16
+#endif
+#ifndef EXEMCL_RT_W12_MAX
+#define EXEMCL_RT_W12_MAX 6
+#endif
+#ifndef EXEMCL_RT16X16_W16
+#define EXEMCL_RT16X16_W16 6
+#endif
+#ifndef EXEMCL_RT16X16_BIG3_NKB
+#define EXEMCL_RT16X16_BIG3_NKB 14
+#endif
+constexpr int w12_rt(int nkb) {
+    const int r = EXEMCL_W12_A_BLOCKS / nkb < EXEMCL_RT_W12_MAX ? EXEMCL_W12_A_BLOCKS / nkb : EXEMCL_RT_W12_MAX;
+    return r > EXEMCL_RT16X16_SMALL ? r : EXEMCL_RT16X16_SMALL;
+}
+
 // Row tiles per wavefront and wavefronts per workgroup for a k-block bucket,
 // as functions of (element bytes, tile, k-blocks) so that the host-side plan
 // (mfma_plan) and the compiled instantiations follow one rule.
@@ -1077,7 +1104,9 @@ constexpr int plan_rt(int elem_bytes, int tile, int nkb) {
     if (tile == 16)
         return elem_bytes == 4            ? 1
                : (nkb >= EXEMCL_WIDE16_MIN_NKB && nkb <= EXEMCL_RT16X16_NKB) ? wide16_rt(nkb)
-               : nkb <= EXEMCL_RT16X16_NKB ? EXEMCL_RT16X16_SMALL
+               : nkb <= EXEMCL_W16_MAX_NKB ? EXEMCL_RT16X16_W16
+               : nkb <= EXEMCL_RT16X16_NKB ? w12_rt(nkb)
+               : nkb <= EXEMCL_RT16X16_BIG3_NKB ? 3
                : nkb <= 16                 ? EXEMCL_RT16X16_BIG
                                            : 1;  // 512 < d <= 1024: one row tile of 32 k-blocks
     if (elem_bytes == 4) return nkb <= EXEMCL_RT1_NKB32 ? 1 : nkb <= 16 ? 2 : 1;
