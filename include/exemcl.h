@@ -23,8 +23,14 @@
  *     the next calls on the same stream (up to 4 per stream, for the 8 most
  *     recently used streams), so repeated calls allocate nothing.  Kept
  *     blocks are released when those limits are exceeded or when an
- *     allocation fails (after waiting for the device), never while a call
- *     uses them.  Calls on different streams may run concurrently; calls on
+ *     allocation fails, never while a call uses them.  Releasing the blocks
+ *     of another stream (a call on a ninth stream of the device evicts the
+ *     least recently used one; a failed allocation releases every free
+ *     block) waits for the whole device (hipDeviceSynchronize) inside that
+ *     call, since the other stream may no longer exist: such a call blocks
+ *     the host until all queued work on the device is done.  Callers that
+ *     need every call to return at once keep to at most 8 streams per
+ *     device.  Calls on different streams may run concurrently; calls on
  *     one stream from several host threads are safe.  Kept blocks are keyed
  *     by the stream's handle, and a new stream can get the handle of a
  *     destroyed one: synchronise a stream before destroying it while calls

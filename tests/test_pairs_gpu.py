@@ -2,10 +2,10 @@
 k-block and one member each; two tiles of a set group folded with one max3
 per element, a lone tile with one max).
 
-Stages hold 19 tiles, so a stage ends with a lone tile, and a set group of
-odd k ends with one too; k = 2 fits a single pair, k = 32 spans two stages,
+Stages hold an even number of tiles (20 here), so only a set group of odd
+k ends with a lone tile; k = 2 fits a single pair, k = 32 spans two stages,
 and with EXEMCL_WG_TARGET=1 a workgroup walks every set group, so groups end
-inside stages.  Every result is compared with the oracle on the rounded
+inside stages and, for odd k, pairs restart mid-stage.  Every result is compared with the oracle on the rounded
 inputs at EXACT_RTOL.
 
 The clamp-form value is a maximum over a set's members, so repeating a
