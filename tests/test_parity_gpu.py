@@ -112,7 +112,7 @@ def test_tiny_workload(torch_gpu, orc, monkeypatch, path):
 # Ragged sizes across tiles: n not a multiple of any row block, l spanning
 # several set groups with a partial last one, every d bucket incl. ragged d.
 # ---------------------------------------------------------------------------
-DIMS = [1, 2, 3, 5, 8, 13, 16, 17, 31, 32, 33, 64, 100, 127, 128, 200, 256, 300, 512]
+DIMS = [1, 2, 3, 5, 8, 13, 16, 17, 31, 32, 33, 64, 80, 96, 100, 127, 128, 200, 256, 300, 400, 448, 512]
 
 
 @pytest.mark.parametrize("prec", ["fp32", "fp16", "bf16"])
@@ -137,7 +137,7 @@ def test_ragged_valu(torch_gpu, orc, monkeypatch, prec, d):
 
 
 @pytest.mark.parametrize("prec", ["fp16", "bf16"])
-@pytest.mark.parametrize("d", [2, 16, 64, 100, 128, 200, 256, 300, 512])
+@pytest.mark.parametrize("d", [2, 16, 64, 96, 100, 128, 200, 256, 300, 448, 512])
 def test_half_inputs_are_exact_in_fp32(torch_gpu, orc, prec, d):
     """fp16/bf16 products are exact in fp32, so against the oracle on the
     rounded inputs the error is fp32 accumulation only.  At d <= 16 the bias
