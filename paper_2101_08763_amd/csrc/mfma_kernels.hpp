@@ -330,7 +330,7 @@ __global__ __launch_bounds__(64) void pack_tiles_kernel(const T *__restrict__ V,
 // per SIMD either way): the CU's eight wavefronts share each staged tile and
 // advance together, and the persistent launch gives every CU equal work.
 #ifndef EXEMCL_WIDE16_MIN_NKB
-#define EXEMCL_WIDE16_MIN_NKB 6
+#define EXEMCL_WIDE16_MIN_NKB 4
 #endif
 #ifndef EXEMCL_WIDE16_WAVES
 #define EXEMCL_WIDE16_WAVES 8
