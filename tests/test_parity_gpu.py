@@ -152,6 +152,24 @@ def test_half_inputs_are_exact_in_fp32(torch_gpu, orc, prec, d):
     exact(got, want, f"{prec} d={d} vs rounded-input oracle")
 
 
+@pytest.mark.parametrize("prec", ["fp32", "fp16", "bf16"])
+@pytest.mark.parametrize("d", [65, 97, 160, 161, 192, 193, 224, 225, 257, 449])
+def test_plan_boundaries_exact(torch_gpu, orc, prec, d):
+    """Both sides of every change of plan: for fp16/bf16 two-member tiles 12
+    vs 8 wavefronts (3 | 4 k-blocks), the row tiles per wavefront (6, 5, 4,
+    3, 2 as the k-blocks grow), a last half k-block (d mod 32 in (0, 16],
+    d <= 192) against a zero-padded one (d > 192), 448 | 449; for fp32 4 vs
+    8 wavefronts (64 | 65) and the 32x32x2 | 16x16x4 change (256 | 257)."""
+    n, l, k = 2711, 45, 6
+    p = synth.random_problem(n, d, l, k, seed=8100 + d, clusters=4)
+    say(f"plan boundary prec={prec} n={n} d={d} l={l} k={k}")
+    Vg, X64 = to_gpu(torch_gpu, p.X, prec)
+    got = gpu_eval(torch_gpu, Vg, p.sets)
+    want = orc.eval(X64, p.sets, 8)
+    check(got, want, orc.loss_e0(X64), prec, f"d={d}")
+    exact(got, want, f"{prec} d={d} vs rounded-input oracle")
+
+
 # ---------------------------------------------------------------------------
 # Full-size workloads (the benchmark's launch configuration) on all or on a
 # strided sample of sets.
