@@ -395,7 +395,7 @@ constexpr int tiles_per_stage() {
     int tps = FILL ? EXEMCL_TPS_FILL_MAX
                    : NFRAG <= EXEMCL_BIG_NKB ? (EXEMCL_STAGE_MIN / TB > 1 ? EXEMCL_STAGE_MIN / TB : 1) : EXEMCL_TPS_BIG;
     constexpr int budget = FILL ? kLdsBytes - kWgSumLds : lds_budget<WAVES>();
-    if (EVEN && (tps & 1)) tps = 2 * round_stage<NFRAG, WAVES>((tps + 1) * TB) <= budget ? tps + 1 : tps - 1;
+    if (EVEN && (tps & 1)) tps = 2 * round_stage<NFRAG, WAVES>((tps + 1) * TB) <= budget ? tps + 1 : tps > 1 ? tps - 1 : tps;
     while (tps > 1 && 2 * round_stage<NFRAG, WAVES>(tps * TB) > budget) tps -= (EVEN && tps > 2) ? 2 : 1;
     return tps;
 }
